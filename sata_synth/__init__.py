@@ -1,0 +1,68 @@
+"""Seeded synthetic inputs shared by the tests, the benchmark and the smoke check.
+
+This module holds no arithmetic of the attention method: it only draws
+i.i.d. N(0, 1) queries, keys and values (the paper's synthetic protocol,
+App. A3) and rounds them to the storage precision.
+
+Recipe.  Every (workload, batch b, head h, tensor) gets its own stream
+``numpy.random.default_rng([SEED, workload, b, h, tensor])`` so that any head
+can be regenerated alone.  Values are drawn in float64, rounded to float32
+(round to nearest even) and, for bf16 workloads, from float32 to bfloat16
+(round to nearest even).  The arrays returned are float32 holding exactly the
+values that the GPU receives, so the oracle sees the same inputs bit for bit.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+SEED = 260200294
+TENSOR_Q, TENSOR_K, TENSOR_V = 0, 1, 2
+
+__all__ = ["SEED", "round_to_bf16", "bf16_bits", "head_stream", "make_qkv", "make_head"]
+
+
+def round_to_bf16(x) -> np.ndarray:
+    """float32 -> nearest bfloat16 value (ties to even), returned as float32.
+
+    NaN and infinities never occur in these inputs and are not treated specially.
+    """
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    bits = x.view(np.uint32).astype(np.uint64)
+    lsb = (bits >> 16) & 1
+    rounded = ((bits + 0x7FFF + lsb) >> 16) << 16
+    return rounded.astype(np.uint32).view(np.float32).reshape(x.shape)
+
+
+def bf16_bits(x) -> np.ndarray:
+    """Upper 16 bits of float32 values that are already bfloat16-representable."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    return (x.view(np.uint32) >> 16).astype(np.uint16)
+
+
+def head_stream(workload: int, b: int, h: int, tensor: int, shape, dtype: str = "f32") -> np.ndarray:
+    """One tensor of one head: N(0,1) of the given shape, rounded to ``dtype``."""
+    rng = np.random.default_rng([SEED, int(workload), int(b), int(h), int(tensor)])
+    x = rng.standard_normal(shape).astype(np.float32)
+    if dtype == "bf16":
+        x = round_to_bf16(x)
+    elif dtype != "f32":
+        raise ValueError(f"unknown dtype {dtype!r}")
+    return x
+
+
+def make_head(workload: int, b: int, h: int, n: int, d_k: int, d_v: int, dtype: str = "f32"):
+    """(q [n, d_k], k [n, d_k], v [n, d_v]) for one head."""
+    return (head_stream(workload, b, h, TENSOR_Q, (n, d_k), dtype),
+            head_stream(workload, b, h, TENSOR_K, (n, d_k), dtype),
+            head_stream(workload, b, h, TENSOR_V, (n, d_v), dtype))
+
+
+def make_qkv(workload: int, B: int, H: int, n: int, d_k: int, d_v: int, dtype: str = "f32"):
+    """(q [B,H,n,d_k], k [B,H,n,d_k], v [B,H,n,d_v]) as float32 arrays."""
+    q = np.empty((B, H, n, d_k), np.float32)
+    k = np.empty((B, H, n, d_k), np.float32)
+    v = np.empty((B, H, n, d_v), np.float32)
+    for b in range(B):
+        for h in range(H):
+            q[b, h], k[b, h], v[b, h] = make_head(workload, b, h, n, d_k, d_v, dtype)
+    return q, k, v
