@@ -1,0 +1,122 @@
+/*
+ * sata.h - C ABI of the MI355X (gfx950) implementation of symmetry-aware Taylor
+ * attention (Heinsen & Kozachkov, "Self-Attention at Constant Cost per Token via
+ * Symmetry-Aware Taylor Approximation", arXiv 2602.00294).
+ *
+ * The method replaces exp(q.k / sqrt(d_k)) in causal attention by its P-term
+ * Taylor series f_P (degrees 0..P-1, Sec. 2.1 and the truncation of Sec. 2.4),
+ * and evaluates the series as an inner product of feature vectors over the
+ * minimal symmetric monomial basis (Sec. 2.3-2.4): D = C(d_k+P-1, P-1) features.
+ * Attention then runs as linear attention over the constant-size state
+ *     S = sum_t phi(k_t) (x) [v_t, 1]        ([D][d_v+1] per head, App. A2)
+ * with y_T = (phi(q_T)^T S_T)[0:d_v] / (phi(q_T)^T S_T)[d_v].
+ *
+ * Conventions fixed by this library (the paper leaves them open):
+ *  - Feature order: degree-major; inside degree p the non-decreasing index tuples
+ *    i1 <= ... <= ip (0-based) in lexicographic order.  Feature 0 is degree 0.
+ *  - Feature weights: phi_m(x) = prod_j x[m_j] / (d^(p/4) * sqrt(prod_c c!)),
+ *    i.e. sqrt(alpha_p * C_p[m]) with alpha_p = 1/(p! d^(p/2)) and C_p[m] the
+ *    permutation count of m; so phi(q).phi(k) = f_P(q.k / sqrt(d)).
+ *  - State layout: [B][H][D][d_v+1] float32, row-major; column d_v holds the
+ *    normaliser Z = sum_t phi(k_t).
+ *  - Causality is inclusive: output T sees tokens 0..T.
+ *
+ * Common rules for every call below:
+ *  - Tensor arguments are device pointers to caller-owned, contiguous, row-major
+ *    memory on the current HIP device.  Activations (q, k, v, y) use the layout
+ *    [B][H][n][d] (prefill) or [B][H][d] (decode).  Outputs must not alias inputs.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Calls are
+ *    asynchronous on that stream and never synchronise the host.
+ *  - Arguments are validated on the host before anything is launched; on any
+ *    error return nothing has been written and sata_last_error() explains it.
+ *  - The library owns only per-device caches (feature tables, workspaces),
+ *    created on first use and freed by sata_release().  Calls made concurrently
+ *    on one device from different streams get separate workspaces.
+ *  - Sizes: 1 <= d_k, d_v <= 255, 1 <= P <= 8, B*H <= 65535, and at most 2^26
+ *    features per head (SATA_ERR_TOO_LARGE beyond).
+ *  - Results are deterministic: identical inputs give bitwise-identical outputs
+ *    (no floating-point atomics).
+ */
+#ifndef SATA_H
+#define SATA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SATA_OK = 0,
+  SATA_ERR_INVALID_ARG = -1, /* null pointer, non-positive size, bad enum        */
+  SATA_ERR_UNSUPPORTED = -2, /* valid request this implementation does not do    */
+  SATA_ERR_TOO_LARGE = -3,   /* feature count / state too large for the kernels  */
+  SATA_ERR_HIP = -4          /* a HIP runtime call or kernel launch failed       */
+} sata_status;
+
+typedef enum {
+  SATA_F32 = 0,  /* IEEE binary32                          */
+  SATA_BF16 = 1  /* bfloat16 (upper half of binary32 bits) */
+} sata_dtype;
+
+/* Number of features D = C(d+P-1, P-1) of degrees 0..P-1 over d coordinates
+ * (Sec. 2.6, hidden state size).  Host only.  -1 if d < 1, P < 1, or overflow. */
+int64_t sata_feature_count(int d, int P);
+
+/* Elements of one head's state, (d_v+1) * C(d_k+P-1, P-1) (Sec. 2.6).
+ * Host only.  -1 on invalid arguments or overflow. */
+int64_t sata_state_elems(int d_k, int d_v, int P);
+
+/* Which monomial feature f is (the rows of the constant index matrix M_p,
+ * Sec. 2.4): writes its degree p to *degree and its indices i1 <= ... <= ip
+ * (0-based) to idx[0..p-1]; idx must hold P-1 ints.  Host only, no GPU use.
+ * SATA_ERR_INVALID_ARG if f is out of range or a pointer is NULL. */
+sata_status sata_feature_index(int d, int P, int64_t f, int* degree, int* idx);
+
+/* Feature map phi (Sec. 2.4, "Efficient Computation", with degree 0 from App. A1).
+ *   x   : [rows][d] of dtype xt (device)
+ *   phi : [rows][D] float32 (device, written)
+ * rows = 0 is a no-op.  Supports 1 <= d <= 255, 1 <= P <= 8. */
+sata_status sata_feature_map(const void* x, sata_dtype xt, int64_t rows, int d, int P,
+                             float* phi, void* stream);
+
+/* Causal prefill over n tokens from an empty state (App. A2: the accumulated
+ * states and their readout; evaluated as a chunked scan).
+ *   q, k : [B][H][n][d_k], v : [B][H][n][d_v], dtype dt (device)
+ *   y    : [B][H][n][d_v], dtype dt (device, written): y_T = S_T / Z_T
+ *   S_out: [B][H][D][d_v+1] float32 (device, written) or NULL: the state after
+ *          token n-1, ready for sata_decode_step.
+ * chunk: tokens per scan block, one of 16, 32, 64, 128.  The result does not
+ * depend on it beyond float rounding.  n = 0 writes a zero S_out and no y.
+ * Intermediate arithmetic is float32 (bf16 operands with float32 accumulation
+ * on the matrix cores for bf16 inputs); the state is always float32. */
+sata_status sata_prefill(const void* q, const void* k, const void* v, sata_dtype dt,
+                         int B, int H, int n, int d_k, int d_v, int P, int chunk,
+                         void* y, float* S_out, void* stream);
+
+/* One decode step for every (b, h) (App. A2, the linear recurrences for Z_{p,T}
+ * and S_{p,T}, then the readout at q_T): S += phi(k) (x) [v, 1], then
+ * y = (phi(q)^T S)[0:d_v] / (phi(q)^T S)[d_v].  The update comes first, so the
+ * new token attends to itself.
+ *   S    : [B][H][D][d_v+1] float32 (device, read and written in place)
+ *   q, k : [B][H][d_k], v : [B][H][d_v], dtype dt (device)
+ *   y    : [B][H][d_v], dtype dt (device, written) */
+sata_status sata_decode_step(float* S, const void* q, const void* k, const void* v,
+                             sata_dtype dt, int B, int H, int d_k, int d_v, int P,
+                             void* y, void* stream);
+
+/* Static text for a status code. */
+const char* sata_status_string(sata_status s);
+
+/* Detail of the last error returned on the calling thread ("" if none). */
+const char* sata_last_error(void);
+
+/* Frees every cached table and workspace on every device.  Must not be called
+ * while work issued by this library is still running. */
+void sata_release(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SATA_H */

@@ -1,0 +1,194 @@
+"""ctypes binding of libsata.so: argument marshalling only.
+
+Every computation runs in the library's HIP kernels.  Torch is used for device
+memory (output allocation) and for the current stream.  If the library has
+not been built, loading fails with an error; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional, Tuple
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG_DIR, "libsata.so")
+HEADER_PATH = os.path.join(os.path.dirname(PKG_DIR), "include", "sata.h")
+
+SATA_F32, SATA_BF16 = 0, 1
+SATA_OK = 0
+
+_lib = None
+
+
+class SataError(RuntimeError):
+    def __init__(self, status: int, func: str, detail: str):
+        super().__init__(f"{func} failed with status {status}: {detail}")
+        self.status = status
+
+
+def load_library(path: Optional[str] = None) -> ctypes.CDLL:
+    """Loads libsata.so once and declares every signature of include/sata.h."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} is missing: build it first with __graft_entry__.build() "
+                           "or python -m paper_2602_00294_amd.build")
+    lib = ctypes.CDLL(p)
+    i32, i64, vp = ctypes.c_int, ctypes.c_int64, ctypes.c_void_p
+    lib.sata_feature_count.argtypes = [i32, i32]
+    lib.sata_feature_count.restype = i64
+    lib.sata_state_elems.argtypes = [i32, i32, i32]
+    lib.sata_state_elems.restype = i64
+    lib.sata_feature_index.argtypes = [i32, i32, i64, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+    lib.sata_feature_index.restype = i32
+    lib.sata_feature_map.argtypes = [vp, i32, i64, i32, i32, vp, vp]
+    lib.sata_feature_map.restype = i32
+    lib.sata_prefill.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp]
+    lib.sata_prefill.restype = i32
+    lib.sata_decode_step.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp]
+    lib.sata_decode_step.restype = i32
+    lib.sata_status_string.argtypes = [i32]
+    lib.sata_status_string.restype = ctypes.c_char_p
+    lib.sata_last_error.argtypes = []
+    lib.sata_last_error.restype = ctypes.c_char_p
+    lib.sata_release.argtypes = []
+    lib.sata_release.restype = None
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def header_functions(path: str = HEADER_PATH):
+    """Names of the functions that include/sata.h declares."""
+    text = open(path).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sata_[a-z_]+)\s*\(", text)))
+
+
+def _check(status: int, func: str):
+    if status != SATA_OK:
+        detail = load_library().sata_last_error().decode()
+        raise SataError(status, func, detail)
+
+
+def feature_count(d: int, P: int) -> int:
+    return int(load_library().sata_feature_count(d, P))
+
+
+def state_elems(d_k: int, d_v: int, P: int) -> int:
+    return int(load_library().sata_state_elems(d_k, d_v, P))
+
+
+def feature_index(d: int, P: int, f: int) -> Tuple[int, ...]:
+    """Index tuple (i1 <= ... <= ip) of feature f in the library's feature order."""
+    deg = ctypes.c_int(0)
+    idx = (ctypes.c_int * max(1, P - 1))()
+    _check(load_library().sata_feature_index(d, P, f, ctypes.byref(deg), idx), "sata_feature_index")
+    return tuple(idx[j] for j in range(deg.value))
+
+
+# ------------------------------------------------------------------ tensor calls
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return SATA_F32
+    if t.dtype == torch.bfloat16:
+        return SATA_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
+
+
+def _check_tensor(t, name: str):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _stream_ptr():
+    return ctypes.c_void_p(_torch().cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None and t.numel() > 0 else ctypes.c_void_p(None)
+
+
+def feature_map(x, P: int):
+    """phi(x) for x [..., d] (float32 or bfloat16) -> float32 [..., D]."""
+    torch = _torch()
+    _check_tensor(x, "x")
+    d = x.shape[-1]
+    rows = x.numel() // d if d else 0
+    D = feature_count(d, P)
+    if D < 0:
+        raise ValueError("invalid d or P")
+    phi = torch.empty(*x.shape[:-1], D, dtype=torch.float32, device=x.device)
+    _check(load_library().sata_feature_map(_ptr(x), _dtype_code(x), rows, d, P, _ptr(phi), _stream_ptr()),
+           "sata_feature_map")
+    return phi
+
+
+def prefill(q, k, v, P: int, chunk: int = 64, want_state: bool = True, y=None, S=None):
+    """Causal prefill.  q, k: [B, H, n, d_k]; v: [B, H, n, d_v].
+
+    Returns (y [B, H, n, d_v] in the input dtype, S [B, H, D, d_v+1] float32 or None).
+    Preallocated outputs may be passed as y= and S=.
+    """
+    torch = _torch()
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check_tensor(t, name)
+    if q.dtype != k.dtype or q.dtype != v.dtype:
+        raise TypeError("q, k, v must share one dtype")
+    B, H, n, dk = q.shape
+    dv = v.shape[-1]
+    if tuple(k.shape) != (B, H, n, dk) or tuple(v.shape[:3]) != (B, H, n):
+        raise ValueError("q, k, v shapes disagree")
+    D = feature_count(dk, P)
+    if y is None:
+        y = torch.empty(B, H, n, dv, dtype=q.dtype, device=q.device)
+    if want_state and S is None:
+        S = torch.empty(B, H, D, dv + 1, dtype=torch.float32, device=q.device)
+    if S is not None:
+        _check_tensor(S, "S")
+        if S.dtype != torch.float32 or tuple(S.shape) != (B, H, D, dv + 1):
+            raise ValueError("S must be float32 [B, H, D, d_v+1]")
+    _check_tensor(y, "y")
+    _check(load_library().sata_prefill(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, H, n, dk, dv, P, chunk,
+                                       _ptr(y), _ptr(S) if S is not None else ctypes.c_void_p(None),
+                                       _stream_ptr()), "sata_prefill")
+    return y, S
+
+
+def decode_step(S, q, k, v, P: int, y=None):
+    """One decode step in place on S [B, H, D, d_v+1]; q, k: [B, H, d_k]; v: [B, H, d_v].
+
+    Returns y [B, H, d_v] in the input dtype.
+    """
+    torch = _torch()
+    for name, t in (("S", S), ("q", q), ("k", k), ("v", v)):
+        _check_tensor(t, name)
+    if S.dtype != torch.float32:
+        raise TypeError("S must be float32")
+    B, H, dk = q.shape
+    dv = v.shape[-1]
+    D = feature_count(dk, P)
+    if tuple(S.shape) != (B, H, D, dv + 1):
+        raise ValueError(f"S must be [B, H, {D}, {dv + 1}]")
+    if y is None:
+        y = torch.empty(B, H, dv, dtype=q.dtype, device=q.device)
+    _check_tensor(y, "y")
+    _check(load_library().sata_decode_step(_ptr(S), _ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, H, dk, dv, P,
+                                           _ptr(y), _stream_ptr()), "sata_decode_step")
+    return y
+
+
+def release():
+    load_library().sata_release()

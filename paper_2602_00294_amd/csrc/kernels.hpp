@@ -1,0 +1,53 @@
+// Internal launch interface between the C ABI layer and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sata {
+
+// One (d, P) feature table resident on a device (see table.hpp for its layout).
+struct DevTable {
+  const uint64_t* packed = nullptr;  // [D] packed multi-indices
+  const float* weight = nullptr;     // [D] feature weights
+  int64_t D = 0;
+  int d = 0;
+  int P = 0;
+};
+
+// ---- feature map -------------------------------------------------------------
+hipError_t launch_feature_map(const void* x, bool bf16, int64_t rows, const DevTable& t,
+                              float* phi, hipStream_t s);
+
+// ---- decode step -------------------------------------------------------------
+struct DecodePlan {
+  int fps = 0;      // features per workgroup slice
+  int nslices = 0;  // slices per head
+  size_t partial_bytes = 0;
+};
+DecodePlan plan_decode(int64_t D, int dv);
+hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, void* y, bool bf16,
+                         int BH, int dk, int dv, const DevTable& t, const DecodePlan& plan,
+                         float* partial, hipStream_t s);
+
+// ---- prefill, generic float32 path --------------------------------------------
+struct PrefillGenericPlan {
+  int fs = 0;        // features per slice
+  int nslices = 0;   // slices per head
+  int seg_len = 0;   // tokens per segment (multiple of the chunk)
+  size_t lds_main = 0;
+  size_t lds_final = 0;
+  size_t partial_bytes = 0;
+};
+// Returns false if no slice size fits the on-chip memory.
+bool plan_prefill_generic(int64_t D, int BH, int n, int dk, int dv, int chunk, size_t max_ws_bytes,
+                          PrefillGenericPlan* plan);
+hipError_t launch_prefill_generic(const void* q, const void* k, const void* v, void* y, bool bf16,
+                                  int BH, int n, int dk, int dv, int chunk, const DevTable& t,
+                                  const PrefillGenericPlan& plan, float* S_state, float* partial,
+                                  hipStream_t s);
+
+// ---- helpers -----------------------------------------------------------------
+hipError_t launch_fill_zero(float* p, int64_t count, hipStream_t s);
+
+}  // namespace sata

@@ -1,0 +1,439 @@
+// Generic float32 kernels: feature map, decode step and a chunked prefill that
+// works for every supported (d_k, d_v, P, chunk) and both input dtypes.
+//
+// Prefill follows the linear-attention form of App. A2 in chunks of C tokens:
+// for chunk c with query rows Q_c, keys K_c and extended values [V_c | 1],
+//     O      = phi(Q_c) S_{c-1}                              (inter-chunk readout)
+//            + mask_{t'<=t}(f_P(Q_c K_c^T / sqrt(d_k))) [V_c | 1]   (intra-chunk)
+//     S_c    = S_{c-1} + phi(K_c)^T [V_c | 1]                (state update)
+//     y      = O[:, :d_v] / O[:, d_v]
+// The state is split over workgroups by feature ranges ("slices"); each slice
+// keeps its part of S in LDS for the whole sequence and writes its partial
+// readout per token; a second kernel adds the slices' partials (in slice
+// order, so the result is deterministic), the intra-chunk term, and divides.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace sata {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+// ---------------------------------------------------------------- feature map
+
+constexpr int kFmRows = 16;
+
+template <typename T>
+__global__ void __launch_bounds__(kThreads)
+feature_map_kernel(const T* __restrict__ x, int64_t rows, int d, const uint64_t* __restrict__ packed,
+                   const float* __restrict__ weight, int64_t D, float* __restrict__ phi) {
+  extern __shared__ float xs[];  // [kFmRows][d]
+  const int64_t r0 = (int64_t)blockIdx.x * kFmRows;
+  const int nr = (int)min<int64_t>(kFmRows, rows - r0);
+  for (int i = threadIdx.x; i < nr * d; i += kThreads) xs[i] = to_f32(x[r0 * d + i]);
+  __syncthreads();
+  const int64_t f = (int64_t)blockIdx.y * kThreads + threadIdx.x;
+  if (f >= D) return;
+  const uint64_t pk = packed[f];
+  const float w = weight[f];
+  for (int r = 0; r < nr; ++r) phi[(r0 + r) * D + f] = feature_value(pk, w, xs + r * d);
+}
+
+// ---------------------------------------------------------------- decode step
+//
+// Workgroup (slice s, head bh) owns features [s*fps, min(D, (s+1)*fps)).  It
+// builds phi(q) and phi(k) for them in LDS, then streams its rows of S once:
+// thread t < R*E (R = rows per pass) handles column j = t % E of row t / E, so
+// consecutive threads touch consecutive addresses; each element is updated
+// (S += phi_k[f] * [v|1][j]) and immediately read out (o_j += phi_q[f] * S).
+
+template <typename T>
+__global__ void __launch_bounds__(kThreads)
+decode_main_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __restrict__ k,
+                   const T* __restrict__ v, T* __restrict__ y, float* __restrict__ partial,
+                   const uint64_t* __restrict__ packed, const float* __restrict__ weight, int64_t D,
+                   int dk, int dv, int fps, int nslices) {
+  extern __shared__ float lds[];
+  const int E = dv + 1;
+  float* xq = lds;               // [dk]
+  float* xk = xq + dk;           // [dk]
+  float* ve = xk + dk;           // [E]
+  float* fq = ve + E;            // [fps]
+  float* fk = fq + fps;          // [fps]
+  float* red = fk + fps;         // [kThreads]
+  const int s = blockIdx.x;
+  const int64_t bh = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int64_t f0 = (int64_t)s * fps;
+  const int nf = (int)min<int64_t>(fps, D - f0);
+
+  for (int i = tid; i < dk; i += kThreads) {
+    xq[i] = to_f32(q[bh * dk + i]);
+    xk[i] = to_f32(k[bh * dk + i]);
+  }
+  for (int i = tid; i < E; i += kThreads) ve[i] = (i < dv) ? to_f32(v[bh * dv + i]) : 1.0f;
+  __syncthreads();
+  for (int f = tid; f < nf; f += kThreads) {
+    const uint64_t pk = packed[f0 + f];
+    const float w = weight[f0 + f];
+    fq[f] = feature_value(pk, w, xq);
+    fk[f] = feature_value(pk, w, xk);
+  }
+  __syncthreads();
+
+  const int R = kThreads / E;  // rows per pass
+  float acc = 0.0f;
+  if (tid < R * E) {
+    const int r = tid / E;
+    const int j = tid - r * E;
+    const float vj = ve[j];
+    float* base = S + (bh * D + f0) * E + j;
+    int f = r;
+    // four rows in flight per thread
+    for (; f + 3 * R < nf; f += 4 * R) {
+      float s0 = base[(int64_t)f * E];
+      float s1 = base[(int64_t)(f + R) * E];
+      float s2 = base[(int64_t)(f + 2 * R) * E];
+      float s3 = base[(int64_t)(f + 3 * R) * E];
+      s0 += fk[f] * vj;
+      s1 += fk[f + R] * vj;
+      s2 += fk[f + 2 * R] * vj;
+      s3 += fk[f + 3 * R] * vj;
+      base[(int64_t)f * E] = s0;
+      base[(int64_t)(f + R) * E] = s1;
+      base[(int64_t)(f + 2 * R) * E] = s2;
+      base[(int64_t)(f + 3 * R) * E] = s3;
+      acc += fq[f] * s0;
+      acc += fq[f + R] * s1;
+      acc += fq[f + 2 * R] * s2;
+      acc += fq[f + 3 * R] * s3;
+    }
+    for (; f < nf; f += R) {
+      float s0 = base[(int64_t)f * E] + fk[f] * vj;
+      base[(int64_t)f * E] = s0;
+      acc += fq[f] * s0;
+    }
+  }
+  red[tid] = acc;
+  __syncthreads();
+  if (tid < E) {
+    float o = 0.0f;
+    for (int r = 0; r < R; ++r) o += red[r * E + tid];
+    red[tid] = o;  // only this thread reads red[r*E + tid] for its own column
+  }
+  __syncthreads();
+  if (nslices == 1) {
+    if (tid < dv) y[bh * dv + tid] = from_f32<T>(red[tid] / red[dv]);
+  } else if (tid < E) {
+    partial[(bh * nslices + s) * E + tid] = red[tid];
+  }
+}
+
+template <typename T>
+__global__ void decode_finalize_kernel(const float* __restrict__ partial, T* __restrict__ y, int dv,
+                                       int nslices) {
+  extern __shared__ float o[];
+  const int E = dv + 1;
+  const int64_t bh = blockIdx.x;
+  for (int j = threadIdx.x; j < E; j += blockDim.x) {
+    float a = 0.0f;
+    for (int s = 0; s < nslices; ++s) a += partial[(bh * nslices + s) * E + j];
+    o[j] = a;
+  }
+  __syncthreads();
+  for (int j = threadIdx.x; j < dv; j += blockDim.x) y[bh * dv + j] = from_f32<T>(o[j] / o[dv]);
+}
+
+// ---------------------------------------------------------------- generic prefill
+
+template <typename T>
+__device__ void load_chunk(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+                           int64_t bh, int n, int t0, int cn, int C, int dk, int dv, float* xq, float* xk,
+                           float* ve) {
+  const int E = dv + 1;
+  const int64_t qoff = (bh * n + t0) * (int64_t)dk;
+  for (int i = threadIdx.x; i < C * dk; i += kThreads) {
+    const int t = i / dk;
+    xq[i] = t < cn ? to_f32(q[qoff + i]) : 0.0f;
+    xk[i] = t < cn ? to_f32(k[qoff + i]) : 0.0f;
+  }
+  const int64_t voff = (bh * n + t0) * (int64_t)dv;
+  for (int i = threadIdx.x; i < C * E; i += kThreads) {
+    const int t = i / E;
+    const int j = i - t * E;
+    float val = 0.0f;
+    if (t < cn) val = (j < dv) ? to_f32(v[voff + (int64_t)t * dv + j]) : 1.0f;
+    ve[i] = val;
+  }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(kThreads)
+prefill_generic_main(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+                     const uint64_t* __restrict__ packed, const float* __restrict__ weight, int64_t D,
+                     float* __restrict__ S_state, float* __restrict__ part, int BH, int n, int dk, int dv,
+                     int C, int FS, int seg0, int seg_len, int first_seg) {
+  extern __shared__ float lds[];
+  const int E = dv + 1;
+  float* Sl = lds;              // [FS][E]
+  float* fb = Sl + FS * E;      // [C][FS]
+  float* xq = fb + C * FS;      // [C][dk]
+  float* xk = xq + C * dk;      // [C][dk]
+  float* ve = xk + C * dk;      // [C][E]
+  const int s = blockIdx.x;
+  const int64_t bh = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int64_t f0 = (int64_t)s * FS;
+  const int fs = (int)min<int64_t>(FS, D - f0);
+  float* Sg = S_state + (bh * D + f0) * E;
+
+  for (int i = tid; i < fs * E; i += kThreads) Sl[i] = first_seg ? 0.0f : Sg[i];
+
+  const int seg_end = min(n, seg0 + seg_len);
+  for (int t0 = seg0; t0 < seg_end; t0 += C) {
+    const int cn = min(C, n - t0);
+    __syncthreads();
+    load_chunk(q, k, v, bh, n, t0, cn, C, dk, dv, xq, xk, ve);
+    __syncthreads();
+    for (int i = tid; i < cn * fs; i += kThreads) {
+      const int t = i / fs;
+      const int f = i - t * fs;
+      fb[t * FS + f] = feature_value(packed[f0 + f], weight[f0 + f], xq + t * dk);
+    }
+    __syncthreads();
+    // inter-chunk readout against the state before this chunk
+    float* pout = part + (((int64_t)s * BH + bh) * seg_len + (t0 - seg0)) * E;
+    for (int o = tid; o < cn * E; o += kThreads) {
+      const int t = o / E;
+      const int j = o - t * E;
+      const float* a = fb + t * FS;
+      float acc = 0.0f;
+      for (int f = 0; f < fs; ++f) acc += a[f] * Sl[f * E + j];
+      pout[o] = acc;
+    }
+    __syncthreads();
+    for (int i = tid; i < cn * fs; i += kThreads) {
+      const int t = i / fs;
+      const int f = i - t * fs;
+      fb[t * FS + f] = feature_value(packed[f0 + f], weight[f0 + f], xk + t * dk);
+    }
+    __syncthreads();
+    // state update with this chunk's keys and values
+    for (int o = tid; o < fs * E; o += kThreads) {
+      const int f = o / E;
+      const int j = o - f * E;
+      float acc = 0.0f;
+      for (int t = 0; t < cn; ++t) acc += fb[t * FS + f] * ve[t * E + j];
+      Sl[o] += acc;
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < fs * E; i += kThreads) Sg[i] = Sl[i];
+}
+
+constexpr int kFinRows = 32;
+
+template <typename T>
+__global__ void __launch_bounds__(kThreads)
+prefill_generic_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+                         const float* __restrict__ part, T* __restrict__ y, int BH, int n, int dk, int dv,
+                         int P, int C, int nslices, int seg0, int seg_len) {
+  extern __shared__ float lds[];
+  const int E = dv + 1;
+  float* xq = lds;                 // [C][dk]
+  float* xk = xq + C * dk;         // [C][dk]
+  float* ve = xk + C * dk;         // [C][E]
+  float* A = ve + C * E;           // [kFinRows][C]
+  float* O = A + kFinRows * C;     // [kFinRows][E]
+  const int64_t bh = blockIdx.y;
+  const int t0 = seg0 + blockIdx.x * C;
+  if (t0 >= n) return;
+  const int cn = min(C, n - t0);
+  const int tid = threadIdx.x;
+  const float scale = 1.0f / sqrtf((float)dk);
+  load_chunk(q, k, v, bh, n, t0, cn, C, dk, dv, xq, xk, ve);
+  __syncthreads();
+  for (int rb = 0; rb < cn; rb += kFinRows) {
+    const int rn = min(kFinRows, cn - rb);
+    for (int i = tid; i < rn * C; i += kThreads) {
+      const int r = i / C;
+      const int tp = i - r * C;
+      const int t = rb + r;
+      float a = 0.0f;
+      if (tp <= t) {
+        float dot = 0.0f;
+        for (int c = 0; c < dk; ++c) dot += xq[t * dk + c] * xk[tp * dk + c];
+        a = taylor_horner(dot * scale, P);
+      }
+      A[i] = a;
+    }
+    __syncthreads();
+    for (int o = tid; o < rn * E; o += kThreads) {
+      const int r = o / E;
+      const int j = o - r * E;
+      const int t = rb + r;
+      float acc = 0.0f;
+      for (int tp = 0; tp <= t; ++tp) acc += A[r * C + tp] * ve[tp * E + j];
+      for (int s = 0; s < nslices; ++s)
+        acc += part[(((int64_t)s * BH + bh) * seg_len + (t0 - seg0) + t) * E + j];
+      O[o] = acc;
+    }
+    __syncthreads();
+    for (int o = tid; o < rn * dv; o += kThreads) {
+      const int r = o / dv;
+      const int j = o - r * dv;
+      y[(bh * n + t0 + rb + r) * (int64_t)dv + j] = from_f32<T>(O[r * E + j] / O[r * E + dv]);
+    }
+    __syncthreads();
+  }
+}
+
+__global__ void fill_zero_kernel(float* p, int64_t count) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) p[i] = 0.0f;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- launchers
+
+hipError_t launch_fill_zero(float* p, int64_t count, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((count + kThreads - 1) / kThreads, 16384);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, s, p, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_feature_map(const void* x, bool bf16, int64_t rows, const DevTable& t, float* phi,
+                              hipStream_t s) {
+  const size_t lds = sizeof(float) * kFmRows * t.d;
+  const int64_t fblocks = (t.D + kThreads - 1) / kThreads;
+  // keep each launch below 2^31 work-items
+  const int64_t max_rb = std::max<int64_t>(1, ((int64_t)1 << 31) / (fblocks * kThreads));
+  const int64_t total_rb = (rows + kFmRows - 1) / kFmRows;
+  for (int64_t rb = 0; rb < total_rb; rb += max_rb) {
+    const int64_t nrb = std::min(max_rb, total_rb - rb);
+    const int64_t r0 = rb * kFmRows;
+    const int64_t nrows = std::min<int64_t>(rows - r0, nrb * kFmRows);
+    dim3 grid((unsigned)nrb, (unsigned)fblocks);
+    if (bf16)
+      hipLaunchKernelGGL(feature_map_kernel<bf16_t>, grid, dim3(kThreads), lds, s,
+                         (const bf16_t*)x + r0 * t.d, nrows, t.d, t.packed, t.weight, t.D, phi + r0 * t.D);
+    else
+      hipLaunchKernelGGL(feature_map_kernel<float>, grid, dim3(kThreads), lds, s,
+                         (const float*)x + r0 * t.d, nrows, t.d, t.packed, t.weight, t.D, phi + r0 * t.D);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+DecodePlan plan_decode(int64_t D, int dv) {
+  const int E = dv + 1;
+  DecodePlan p;
+  // about 32K state elements (128 KB of float32) per workgroup
+  int64_t fps = std::max<int64_t>(kThreads / E, (32768 + E - 1) / E);
+  fps = std::min<int64_t>(fps, 4096);
+  fps = std::min<int64_t>(fps, D);
+  p.fps = (int)fps;
+  p.nslices = (int)((D + fps - 1) / fps);
+  p.partial_bytes = 0;
+  return p;
+}
+
+hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, void* y, bool bf16, int BH,
+                         int dk, int dv, const DevTable& t, const DecodePlan& plan, float* partial,
+                         hipStream_t s) {
+  const int E = dv + 1;
+  const size_t lds = sizeof(float) * (2 * dk + E + 2 * plan.fps + kThreads);
+  dim3 grid((unsigned)plan.nslices, (unsigned)BH);
+  if (bf16)
+    hipLaunchKernelGGL(decode_main_kernel<bf16_t>, grid, dim3(kThreads), lds, s, S, (const bf16_t*)q,
+                       (const bf16_t*)k, (const bf16_t*)v, (bf16_t*)y, partial, t.packed, t.weight, t.D, dk,
+                       dv, plan.fps, plan.nslices);
+  else
+    hipLaunchKernelGGL(decode_main_kernel<float>, grid, dim3(kThreads), lds, s, S, (const float*)q,
+                       (const float*)k, (const float*)v, (float*)y, partial, t.packed, t.weight, t.D, dk, dv,
+                       plan.fps, plan.nslices);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || plan.nslices == 1) return e;
+  const size_t lds2 = sizeof(float) * E;
+  if (bf16)
+    hipLaunchKernelGGL(decode_finalize_kernel<bf16_t>, dim3((unsigned)BH), dim3(64), lds2, s, partial,
+                       (bf16_t*)y, dv, plan.nslices);
+  else
+    hipLaunchKernelGGL(decode_finalize_kernel<float>, dim3((unsigned)BH), dim3(64), lds2, s, partial,
+                       (float*)y, dv, plan.nslices);
+  return hipGetLastError();
+}
+
+static constexpr size_t kLdsBudget = 64 * 1024;
+
+bool plan_prefill_generic(int64_t D, int BH, int n, int dk, int dv, int chunk, size_t max_ws_bytes,
+                          PrefillGenericPlan* plan) {
+  const int E = dv + 1;
+  const int C = chunk;
+  const size_t fixed = sizeof(float) * ((size_t)2 * C * dk + (size_t)C * E);
+  const size_t per_feature = sizeof(float) * ((size_t)E + C);
+  if (fixed + 8 * per_feature > kLdsBudget) return false;
+  int64_t fs = (int64_t)((kLdsBudget - fixed) / per_feature);
+  fs = std::min<int64_t>(fs, 512);
+  fs = std::min<int64_t>(fs, D);
+  plan->fs = (int)fs;
+  plan->nslices = (int)((D + fs - 1) / fs);
+  plan->lds_main = fixed + per_feature * (size_t)fs;
+  plan->lds_final = sizeof(float) * ((size_t)2 * C * dk + (size_t)C * E + (size_t)kFinRows * C +
+                                     (size_t)kFinRows * E);
+  if (plan->lds_final > kLdsBudget) return false;
+  // partial readouts for one segment: [nslices][BH][seg_len][E]
+  const size_t per_token = sizeof(float) * (size_t)plan->nslices * BH * E;
+  int64_t seg = (int64_t)(max_ws_bytes / per_token);
+  seg = (seg / C) * C;
+  if (seg < C) seg = C;
+  const int64_t n_round = ((int64_t)std::max(n, 1) + C - 1) / C * C;
+  plan->seg_len = (int)std::min<int64_t>(seg, n_round);
+  plan->partial_bytes = per_token * (size_t)plan->seg_len;
+  return true;
+}
+
+hipError_t launch_prefill_generic(const void* q, const void* k, const void* v, void* y, bool bf16, int BH,
+                                  int n, int dk, int dv, int chunk, const DevTable& t,
+                                  const PrefillGenericPlan& plan, float* S_state, float* partial,
+                                  hipStream_t s) {
+  const int C = chunk;
+  for (int seg0 = 0; seg0 < n; seg0 += plan.seg_len) {
+    const int first = seg0 == 0 ? 1 : 0;
+    dim3 g1((unsigned)plan.nslices, (unsigned)BH);
+    if (bf16)
+      hipLaunchKernelGGL(prefill_generic_main<bf16_t>, g1, dim3(kThreads), plan.lds_main, s,
+                         (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, t.packed, t.weight, t.D,
+                         S_state, partial, BH, n, dk, dv, C, plan.fs, seg0, plan.seg_len, first);
+    else
+      hipLaunchKernelGGL(prefill_generic_main<float>, g1, dim3(kThreads), plan.lds_main, s,
+                         (const float*)q, (const float*)k, (const float*)v, t.packed, t.weight, t.D, S_state,
+                         partial, BH, n, dk, dv, C, plan.fs, seg0, plan.seg_len, first);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int seg_tokens = std::min(plan.seg_len, n - seg0);
+    dim3 g2((unsigned)((seg_tokens + C - 1) / C), (unsigned)BH);
+    if (bf16)
+      hipLaunchKernelGGL(prefill_generic_finalize<bf16_t>, g2, dim3(kThreads), plan.lds_final, s,
+                         (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, partial, (bf16_t*)y, BH, n,
+                         dk, dv, t.P, C, plan.nslices, seg0, plan.seg_len);
+    else
+      hipLaunchKernelGGL(prefill_generic_finalize<float>, g2, dim3(kThreads), plan.lds_final, s,
+                         (const float*)q, (const float*)k, (const float*)v, partial, (float*)y, BH, n, dk,
+                         dv, t.P, C, plan.nslices, seg0, plan.seg_len);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace sata

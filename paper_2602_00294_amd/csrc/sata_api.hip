@@ -1,0 +1,309 @@
+// C ABI of the library: argument validation, per-device caches of feature
+// tables and workspaces, and dispatch to the HIP kernels.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "kernels.hpp"
+#include "prefill_mfma.hpp"
+#include "sata.h"
+#include "table.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+sata_status fail(sata_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+sata_status ok() {
+  g_last_error.clear();
+  return SATA_OK;
+}
+
+sata_status hip_fail(hipError_t e, const char* what) {
+  return fail(SATA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+struct TableEntry {
+  sata::FeatureTable host;
+  uint64_t* packed = nullptr;
+  float* weight = nullptr;
+};
+
+struct Workspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+
+struct DeviceCache {
+  std::map<std::pair<int, int>, TableEntry> tables;
+  std::map<hipStream_t, Workspace> workspaces;
+};
+
+std::mutex g_mu;
+std::map<int, DeviceCache> g_devices;
+
+// Upper bound on features per head accepted by the kernels.
+constexpr int64_t kMaxFeatures = (int64_t)1 << 26;
+// Upper bound on B*H (one grid dimension per head).
+constexpr int kMaxHeads = 65535;
+// Upper bound on the partial-readout workspace one call may use.
+constexpr size_t kMaxWorkspace = (size_t)512 << 20;
+
+sata_status get_table(int d, int P, hipStream_t stream, sata::DevTable* out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lock(g_mu);
+  DeviceCache& dc = g_devices[dev];
+  auto key = std::make_pair(d, P);
+  auto it = dc.tables.find(key);
+  if (it == dc.tables.end()) {
+    TableEntry ent;
+    ent.host = sata::build_table(d, P);
+    const size_t D = (size_t)ent.host.D;
+    if ((e = hipMalloc(&ent.packed, D * sizeof(uint64_t))) != hipSuccess) return hip_fail(e, "hipMalloc(table)");
+    if ((e = hipMalloc(&ent.weight, D * sizeof(float))) != hipSuccess) {
+      hipFree(ent.packed);
+      return hip_fail(e, "hipMalloc(table)");
+    }
+    // The host copy lives in the cache, so an asynchronous copy is safe.
+    e = hipMemcpyAsync(ent.packed, ent.host.packed.data(), D * sizeof(uint64_t), hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(ent.weight, ent.host.weight.data(), D * sizeof(float), hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) {
+      hipFree(ent.packed);
+      hipFree(ent.weight);
+      return hip_fail(e, "uploading feature table");
+    }
+    it = dc.tables.emplace(key, std::move(ent)).first;
+  }
+  out->packed = it->second.packed;
+  out->weight = it->second.weight;
+  out->D = it->second.host.D;
+  out->d = d;
+  out->P = P;
+  return SATA_OK;
+}
+
+// Returns a per-(device, stream) scratch buffer of at least `bytes`.
+sata_status get_workspace(size_t bytes, hipStream_t stream, void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lock(g_mu);
+  Workspace& ws = g_devices[dev].workspaces[stream];
+  if (ws.bytes < bytes) {
+    if (ws.ptr) {
+      // earlier work on this stream may still read the old buffer
+      if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+      hipFree(ws.ptr);
+      ws.ptr = nullptr;
+      ws.bytes = 0;
+    }
+    size_t want = bytes < ((size_t)1 << 20) ? ((size_t)1 << 20) : bytes;
+    if ((e = hipMalloc(&ws.ptr, want)) != hipSuccess) return hip_fail(e, "hipMalloc(workspace)");
+    ws.bytes = want;
+  }
+  *out = ws.ptr;
+  return SATA_OK;
+}
+
+bool valid_dtype(sata_dtype t) { return t == SATA_F32 || t == SATA_BF16; }
+
+sata_status check_dims(int d_k, int d_v, int P, int64_t* D) {
+  if (d_k < 1 || d_k > sata::kMaxDim) return fail(SATA_ERR_INVALID_ARG, "d_k=%d outside 1..%d", d_k, sata::kMaxDim);
+  if (d_v < 1 || d_v > sata::kMaxDim) return fail(SATA_ERR_INVALID_ARG, "d_v=%d outside 1..%d", d_v, sata::kMaxDim);
+  if (P < 1 || P > sata::kMaxP) return fail(SATA_ERR_INVALID_ARG, "P=%d outside 1..%d", P, sata::kMaxP);
+  const int64_t f = sata::feature_count(d_k, P);
+  if (f < 0 || f > kMaxFeatures)
+    return fail(SATA_ERR_TOO_LARGE, "C(d_k+P-1, P-1) features exceed %lld", (long long)kMaxFeatures);
+  *D = f;
+  return SATA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t sata_feature_count(int d, int P) {
+  if (d < 1 || P < 1) return -1;
+  return sata::feature_count(d, P);
+}
+
+int64_t sata_state_elems(int d_k, int d_v, int P) {
+  if (d_k < 1 || d_v < 1 || P < 1) return -1;
+  const int64_t f = sata::feature_count(d_k, P);
+  if (f < 0 || f > INT64_MAX / (d_v + 1)) return -1;
+  return f * (d_v + 1);
+}
+
+sata_status sata_feature_index(int d, int P, int64_t f, int* degree, int* idx) {
+  if (!degree || !idx) return fail(SATA_ERR_INVALID_ARG, "null output pointer");
+  if (d < 1 || d > sata::kMaxDim || P < 1 || P > sata::kMaxP)
+    return fail(SATA_ERR_INVALID_ARG, "d=%d or P=%d out of range", d, P);
+  const int64_t D = sata::feature_count(d, P);
+  if (D < 0 || f < 0 || f >= D) return fail(SATA_ERR_INVALID_ARG, "feature %lld out of range", (long long)f);
+  // skip whole degrees, then walk the tuples of the degree that holds f
+  int64_t base = 0;
+  for (int p = 0; p < P; ++p) {
+    const int64_t m = sata::binom((int64_t)d + p - 1, p);
+    if (f < base + m) {
+      int64_t i = base;
+      bool found = false;
+      if (p == 0) found = true;
+      else
+        sata::for_each_tuple(d, p, [&](const int* t) {
+          if (!found && i == f) {
+            for (int j = 0; j < p; ++j) idx[j] = t[j];
+            found = true;
+          }
+          ++i;
+        });
+      *degree = p;
+      return ok();
+    }
+    base += m;
+  }
+  return fail(SATA_ERR_INVALID_ARG, "feature %lld out of range", (long long)f);
+}
+
+sata_status sata_feature_map(const void* x, sata_dtype xt, int64_t rows, int d, int P, float* phi,
+                             void* stream) {
+  if (!valid_dtype(xt)) return fail(SATA_ERR_INVALID_ARG, "unknown dtype %d", (int)xt);
+  if (rows < 0) return fail(SATA_ERR_INVALID_ARG, "rows=%lld < 0", (long long)rows);
+  int64_t D = 0;
+  sata_status st = check_dims(d, 1, P, &D);
+  if (st != SATA_OK) return st;
+  if (rows == 0) return ok();
+  if (!x || !phi) return fail(SATA_ERR_INVALID_ARG, "null tensor pointer");
+  hipStream_t s = (hipStream_t)stream;
+  sata::DevTable t;
+  if ((st = get_table(d, P, s, &t)) != SATA_OK) return st;
+  hipError_t e = sata::launch_feature_map(x, xt == SATA_BF16, rows, t, phi, s);
+  if (e != hipSuccess) return hip_fail(e, "feature_map launch");
+  return ok();
+}
+
+sata_status sata_prefill(const void* q, const void* k, const void* v, sata_dtype dt, int B, int H, int n,
+                         int d_k, int d_v, int P, int chunk, void* y, float* S_out, void* stream) {
+  if (!valid_dtype(dt)) return fail(SATA_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
+  if (B < 1 || H < 1) return fail(SATA_ERR_INVALID_ARG, "B=%d H=%d must be >= 1", B, H);
+  if (n < 0) return fail(SATA_ERR_INVALID_ARG, "n=%d < 0", n);
+  int64_t D = 0;
+  sata_status st = check_dims(d_k, d_v, P, &D);
+  if (st != SATA_OK) return st;
+  if (chunk != 16 && chunk != 32 && chunk != 64 && chunk != 128)
+    return fail(SATA_ERR_UNSUPPORTED, "chunk=%d; supported: 16, 32, 64, 128", chunk);
+  if ((int64_t)B * H > kMaxHeads) return fail(SATA_ERR_TOO_LARGE, "B*H=%lld exceeds %d", (long long)B * H, kMaxHeads);
+  if (n > 0 && (!q || !k || !v || !y)) return fail(SATA_ERR_INVALID_ARG, "null tensor pointer");
+  const int BH = B * H;
+  const int E = d_v + 1;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e;
+  if (n == 0) {
+    if (S_out) {
+      if ((e = sata::launch_fill_zero(S_out, (int64_t)BH * D * E, s)) != hipSuccess)
+        return hip_fail(e, "fill launch");
+    }
+    return ok();
+  }
+  sata::DevTable t;
+  if ((st = get_table(d_k, P, s, &t)) != SATA_OK) return st;
+
+  // bf16 fast path on the matrix cores where a tuned kernel exists
+  sata::MfmaPrefillPlan mp;
+  if (dt == SATA_BF16 && sata::plan_prefill_mfma(BH, n, d_k, d_v, P, chunk, &mp)) {
+    void* ws = nullptr;
+    if ((st = get_workspace(mp.workspace_bytes, s, &ws)) != SATA_OK) return st;
+    e = sata::launch_prefill_mfma(q, k, v, y, S_out, BH, n, d_k, d_v, P, chunk, mp, ws, s);
+    if (e != hipSuccess) return hip_fail(e, "prefill (matrix-core) launch");
+    return ok();
+  }
+
+  sata::PrefillGenericPlan plan;
+  if (!sata::plan_prefill_generic(D, BH, n, d_k, d_v, chunk, kMaxWorkspace, &plan))
+    return fail(SATA_ERR_UNSUPPORTED, "no slice size fits on chip for d_k=%d d_v=%d chunk=%d", d_k, d_v, chunk);
+  const size_t state_bytes = S_out ? 0 : sizeof(float) * (size_t)BH * D * E;
+  void* ws = nullptr;
+  if ((st = get_workspace(plan.partial_bytes + state_bytes, s, &ws)) != SATA_OK) return st;
+  float* partial = (float*)ws;
+  float* S_state = S_out ? S_out : (float*)((char*)ws + plan.partial_bytes);
+  e = sata::launch_prefill_generic(q, k, v, y, dt == SATA_BF16, BH, n, d_k, d_v, chunk, t, plan, S_state,
+                                   partial, s);
+  if (e != hipSuccess) return hip_fail(e, "prefill launch");
+  return ok();
+}
+
+sata_status sata_decode_step(float* S, const void* q, const void* k, const void* v, sata_dtype dt, int B,
+                             int H, int d_k, int d_v, int P, void* y, void* stream) {
+  if (!valid_dtype(dt)) return fail(SATA_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
+  if (B < 1 || H < 1) return fail(SATA_ERR_INVALID_ARG, "B=%d H=%d must be >= 1", B, H);
+  int64_t D = 0;
+  sata_status st = check_dims(d_k, d_v, P, &D);
+  if (st != SATA_OK) return st;
+  if ((int64_t)B * H > kMaxHeads) return fail(SATA_ERR_TOO_LARGE, "B*H=%lld exceeds %d", (long long)B * H, kMaxHeads);
+  if (!S || !q || !k || !v || !y) return fail(SATA_ERR_INVALID_ARG, "null tensor pointer");
+  const int BH = B * H;
+  hipStream_t s = (hipStream_t)stream;
+  sata::DevTable t;
+  if ((st = get_table(d_k, P, s, &t)) != SATA_OK) return st;
+  sata::DecodePlan plan = sata::plan_decode(D, d_v);
+  float* partial = nullptr;
+  if (plan.nslices > 1) {
+    void* ws = nullptr;
+    const size_t bytes = sizeof(float) * (size_t)BH * plan.nslices * (d_v + 1);
+    if ((st = get_workspace(bytes, s, &ws)) != SATA_OK) return st;
+    partial = (float*)ws;
+  }
+  hipError_t e = sata::launch_decode(S, q, k, v, y, dt == SATA_BF16, BH, d_k, d_v, t, plan, partial, s);
+  if (e != hipSuccess) return hip_fail(e, "decode launch");
+  return ok();
+}
+
+const char* sata_status_string(sata_status s) {
+  switch (s) {
+    case SATA_OK: return "ok";
+    case SATA_ERR_INVALID_ARG: return "invalid argument";
+    case SATA_ERR_UNSUPPORTED: return "unsupported";
+    case SATA_ERR_TOO_LARGE: return "too large";
+    case SATA_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* sata_last_error(void) { return g_last_error.c_str(); }
+
+void sata_release(void) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  int cur = 0;
+  hipGetDevice(&cur);
+  for (auto& kv : g_devices) {
+    hipSetDevice(kv.first);
+    for (auto& t : kv.second.tables) {
+      hipFree(t.second.packed);
+      hipFree(t.second.weight);
+    }
+    for (auto& w : kv.second.workspaces) hipFree(w.second.ptr);
+  }
+  g_devices.clear();
+  hipSetDevice(cur);
+}
+
+}  // extern "C"

@@ -1,0 +1,95 @@
+"""CPU-side checks of the C ABI: the library loads, exports every declared
+symbol, and its host-only calls and argument validation behave as documented.
+No compute call reaches a GPU here."""
+import ctypes
+import itertools
+import math
+
+import pytest
+
+import oracle
+from paper_2602_00294_amd import _binding as bnd
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return bnd.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = bnd.header_functions()
+    assert {"sata_feature_map", "sata_prefill", "sata_decode_step"} <= set(names)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_feature_and_state_counts(lib):
+    for d in (1, 2, 8, 16, 32, 64):
+        for P in range(1, 8):
+            assert lib.sata_feature_count(d, P) == oracle.feature_count(d, P)
+            assert lib.sata_state_elems(d, 5, P) == oracle.state_elems(d, 5, P)
+    assert lib.sata_feature_count(0, 4) == -1
+    assert lib.sata_feature_count(4, 0) == -1
+
+
+@pytest.mark.parametrize("d,P", [(1, 5), (2, 3), (3, 4), (8, 4), (5, 7), (16, 3)])
+def test_feature_order_matches_oracle(d, P):
+    want = oracle.multi_indices(d, P)
+    got = [bnd.feature_index(d, P, f) for f in range(len(want))]
+    assert got == want
+
+
+def test_feature_index_spot_checks_large():
+    # last feature of degree P-1 is (d-1, ..., d-1); the first of degree 2 is (0, 0)
+    for d, P in ((32, 4), (64, 4), (16, 6)):
+        D = oracle.feature_count(d, P)
+        assert bnd.feature_index(d, P, D - 1) == (d - 1,) * (P - 1)
+        assert bnd.feature_index(d, P, 1 + d) == (0, 0)
+        assert bnd.feature_index(d, P, d) == (d - 1,)
+
+
+def test_feature_index_rejects_out_of_range(lib):
+    deg = ctypes.c_int(0)
+    idx = (ctypes.c_int * 8)()
+    assert lib.sata_feature_index(4, 3, 14, ctypes.byref(deg), idx) == bnd.SATA_OK
+    assert deg.value == 2 and (idx[0], idx[1]) == (3, 3)
+    assert lib.sata_feature_index(4, 3, 15, ctypes.byref(deg), idx) == -1
+    assert lib.sata_feature_index(4, 3, -1, ctypes.byref(deg), idx) == -1
+    assert lib.sata_feature_index(4, 3, 0, None, idx) == -1
+
+
+NULL = ctypes.c_void_p(None)
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+
+
+@pytest.mark.parametrize("args,code", [
+    # (dtype, B, H, n, dk, dv, P, chunk, ptr)
+    ((7, 1, 1, 8, 4, 4, 4, 64, FAKE), -1),       # bad dtype
+    ((0, 0, 1, 8, 4, 4, 4, 64, FAKE), -1),       # B = 0
+    ((0, 1, 1, -1, 4, 4, 4, 64, FAKE), -1),      # n < 0
+    ((0, 1, 1, 8, 0, 4, 4, 64, FAKE), -1),       # d_k = 0
+    ((0, 1, 1, 8, 4, 0, 4, 64, FAKE), -1),       # d_v = 0
+    ((0, 1, 1, 8, 4, 4, 9, 64, FAKE), -1),       # P > 8
+    ((0, 1, 1, 8, 4, 4, 4, 48, FAKE), -2),       # unsupported chunk
+    ((0, 1, 1, 8, 200, 4, 8, 64, FAKE), -3),     # feature count too large
+    ((0, 1, 1, 8, 4, 4, 4, 64, NULL), -1),       # null tensors
+])
+def test_prefill_validation(lib, args, code):
+    dt, B, H, n, dk, dv, P, chunk, ptr = args
+    st = lib.sata_prefill(ptr, ptr, ptr, dt, B, H, n, dk, dv, P, chunk, ptr, NULL, NULL)
+    assert st == code
+    assert lib.sata_last_error().decode() != ""
+
+
+def test_decode_and_feature_map_validation(lib):
+    assert lib.sata_decode_step(NULL, FAKE, FAKE, FAKE, 0, 1, 1, 4, 4, 4, FAKE, NULL) == -1
+    assert lib.sata_decode_step(FAKE, FAKE, FAKE, FAKE, 3, 1, 1, 4, 4, 4, FAKE, NULL) == -1
+    assert lib.sata_decode_step(FAKE, FAKE, FAKE, FAKE, 0, 1, 1, 4, 4, 0, FAKE, NULL) == -1
+    assert lib.sata_feature_map(FAKE, 0, -5, 4, 3, FAKE, NULL) == -1
+    assert lib.sata_feature_map(FAKE, 0, 0, 4, 3, FAKE, NULL) == 0   # rows = 0: no-op
+    assert lib.sata_feature_map(NULL, 0, 3, 4, 3, FAKE, NULL) == -1
+
+
+def test_status_strings(lib):
+    for code in (0, -1, -2, -3, -4):
+        assert lib.sata_status_string(code)

@@ -1,0 +1,165 @@
+"""GPU parity: every hot-path call through the C ABI against the float64 oracle.
+
+Inputs are the seeded synthetic N(0,1) tensors of sata_synth.  Floating-point
+results must match the oracle within relative error 1e-4 (float32 inputs) or
+2e-2 (bfloat16 inputs, float32 state): per query row ||y - y_ref|| / ||y_ref||
+over rows whose denominator does not cancel (kappa <= 100), and
+||S - S_ref||_F / ||S_ref||_F for the state.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import sata_synth as syn
+from gpu_util import TOL, check_prefill_head, to_dev, to_host
+from oracle.metrics import max_row_rel_error, state_rel_error
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def sata():
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    import paper_2602_00294_amd as m
+    m.load_library()
+    return m
+
+
+def _say(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+# ------------------------------------------------------------------ feature map
+
+@pytest.mark.parametrize("d,P,rows,dtype", [
+    (8, 4, 37, "f32"), (16, 4, 100, "bf16"), (3, 7, 19, "f32"), (32, 4, 65, "bf16"),
+    (1, 1, 5, "f32"), (5, 2, 1, "f32"), (64, 3, 33, "f32")])
+def test_feature_map(sata, d, P, rows, dtype):
+    _say(f"feature_map d={d} P={P} rows={rows} {dtype}")
+    x = syn.head_stream(100, d, P, 0, (rows, d), dtype)
+    phi = to_host(sata.feature_map(to_dev(x, dtype), P))
+    ref = oracle.phi_ref(x, P)
+    assert phi.shape == ref.shape
+    np.testing.assert_allclose(phi, ref, rtol=2e-6, atol=1e-30)
+
+
+# ------------------------------------------------------------------ prefill
+
+def _run_prefill(sata, workload, B, H, n, dk, dv, P, chunk, dtype, want_state=True):
+    q, k, v = syn.make_qkv(workload, B, H, n, dk, dv, dtype)
+    y, S = sata.prefill(to_dev(q, dtype), to_dev(k, dtype), to_dev(v, dtype), P, chunk, want_state=want_state)
+    torch.cuda.synchronize()
+    return q, k, v, to_host(y), (to_host(S) if S is not None else None)
+
+
+PREFILL_CASES = [
+    # workload, B, H, n, d_k, d_v, P, chunk, dtype
+    (1, 1, 1, 256, 8, 8, 4, 64, "f32"),       # the single-head n=256 d=8 P=4 case
+    (11, 1, 2, 77, 5, 3, 3, 16, "f32"),
+    (12, 2, 1, 130, 4, 7, 5, 32, "f32"),
+    (13, 1, 1, 1, 8, 8, 4, 64, "f32"),
+    (14, 1, 1, 200, 16, 16, 6, 128, "f32"),
+    (15, 1, 1, 50, 4, 4, 1, 16, "f32"),
+    (16, 2, 2, 65, 8, 8, 2, 64, "bf16"),
+    (17, 1, 3, 129, 16, 16, 4, 64, "bf16"),
+    (18, 1, 2, 300, 32, 32, 4, 64, "bf16"),
+    (19, 1, 1, 97, 2, 9, 7, 32, "f32"),
+]
+
+
+@pytest.mark.parametrize("case", PREFILL_CASES, ids=lambda c: "w{}_B{}H{}n{}dk{}dv{}P{}C{}_{}".format(*c))
+def test_prefill_matches_oracle(sata, case):
+    workload, B, H, n, dk, dv, P, chunk, dtype = case
+    _say(f"prefill {case}")
+    q, k, v, y, S = _run_prefill(sata, *case)
+    assert np.all(np.isfinite(y))
+    for b in range(B):
+        for h in range(H):
+            check_prefill_head(y[b, h], S[b, h], q[b, h], k[b, h], v[b, h], P, dtype, f"{case} b{b} h{h}")
+
+
+def test_prefill_empty_sequence_zeroes_state(sata):
+    S = torch.full((1, 2, oracle.feature_count(4, 3), 6), 7.0, device="cuda")
+    q = torch.empty(1, 2, 0, 4, device="cuda")
+    v = torch.empty(1, 2, 0, 5, device="cuda")
+    y, S2 = sata.prefill(q, q, v, 3, 32, S=S)
+    torch.cuda.synchronize()
+    assert y.numel() == 0 and float(S2.abs().max()) == 0.0
+
+
+def test_prefill_deterministic(sata):
+    q, k, v = syn.make_qkv(20, 1, 2, 333, 16, 16, "bf16")
+    args = [to_dev(a, "bf16") for a in (q, k, v)]
+    y1, S1 = sata.prefill(*args, 4, 64)
+    y2, S2 = sata.prefill(*args, 4, 64)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2) and torch.equal(S1, S2)
+
+
+def test_prefill_chunk_invariance(sata):
+    q, k, v = syn.make_qkv(21, 1, 1, 300, 8, 8, "f32")
+    outs = [sata.prefill(*(to_dev(a, "f32") for a in (q, k, v)), 4, c) for c in (16, 32, 64, 128)]
+    torch.cuda.synchronize()
+    y0, S0 = to_host(outs[0][0]), to_host(outs[0][1])
+    for y, S in outs[1:]:
+        assert max_row_rel_error(to_host(y)[0, 0], y0[0, 0])[0] < 1e-5
+        assert state_rel_error(to_host(S), S0) < 1e-5
+
+
+def test_prefill_rejects_bad_chunk(sata):
+    x = torch.zeros(1, 1, 4, 4, device="cuda")
+    with pytest.raises(sata.SataError):
+        sata.prefill(x, x, x, 3, 48)
+
+
+# ------------------------------------------------------------------ decode
+
+@pytest.mark.parametrize("B,H,n1,n2,d,P,dtype", [
+    (2, 2, 40, 9, 8, 4, "f32"), (1, 3, 64, 5, 16, 4, "bf16"), (1, 1, 0, 6, 4, 3, "f32"),
+    (1, 2, 70, 4, 32, 4, "bf16"), (1, 1, 20, 3, 5, 6, "f32")])
+def test_decode_continues_prefill(sata, B, H, n1, n2, d, P, dtype):
+    _say(f"decode B={B} H={H} n1={n1} n2={n2} d={d} P={P} {dtype}")
+    q, k, v = syn.make_qkv(30 + d, B, H, n1 + n2, d, d, dtype)
+    dev = lambda a: to_dev(a, dtype)
+    D = oracle.feature_count(d, P)
+    if n1 > 0:
+        _, S = sata.prefill(dev(q[:, :, :n1]), dev(k[:, :, :n1]), dev(v[:, :, :n1]), P, 32)
+    else:
+        S = torch.zeros(B, H, D, d + 1, device="cuda")
+    ys = []
+    for t in range(n1, n1 + n2):
+        ys.append(to_host(sata.decode_step(S, dev(q[:, :, t].copy()), dev(k[:, :, t].copy()),
+                                           dev(v[:, :, t].copy()), P)))
+    torch.cuda.synchronize()
+    S_host = to_host(S)
+    for b in range(B):
+        for h in range(H):
+            yr, _, kap = oracle.taylor_attention_rows(q[b, h], k[b, h], v[b, h], P, list(range(n1, n1 + n2)))
+            got = np.stack([yy[b, h] for yy in ys])
+            err, _ = max_row_rel_error(got, yr, kap)
+            assert err <= TOL[dtype], f"b{b} h{h}: {err:.3e}"
+            s_err = state_rel_error(S_host[b, h], oracle.state_ref(k[b, h], v[b, h], P))
+            assert s_err <= TOL[dtype], f"state b{b} h{h}: {s_err:.3e}"
+
+
+def test_decode_large_state_slices(sata):
+    """A state large enough to be split over several workgroups per head."""
+    d, P, B, H = 32, 4, 1, 2
+    q, k, v = syn.make_qkv(40, B, H, 8, d, d, "f32")
+    D = oracle.feature_count(d, P)
+    rng = np.random.default_rng(5)
+    S0 = rng.standard_normal((B, H, D, d + 1)).astype(np.float32)
+    S0[..., d] = np.abs(S0[..., d]) + 50.0       # a comfortably positive normaliser
+    S = torch.from_numpy(S0).cuda()
+    y = to_host(sata.decode_step(S, to_dev(q[:, :, 0].copy(), "f32"), to_dev(k[:, :, 0].copy(), "f32"),
+                                 to_dev(v[:, :, 0].copy(), "f32"), P))
+    torch.cuda.synchronize()
+    for h in range(H):
+        yr, Sr = oracle.decode_ref(S0[0, h], q[0, h, :1], k[0, h, :1], v[0, h, :1], P)
+        assert max_row_rel_error(y[0, h][None], yr)[0] < 1e-4
+        assert state_rel_error(to_host(S)[0, h], Sr) < 1e-6
