@@ -1,0 +1,227 @@
+"""Benchmark: causal prefill then decode of symmetry-aware Taylor attention on one MI355X.
+
+Workload (d_k = d_v = 32, P = 4, D = 6545 features, bf16 q/k/v, float32 state):
+  prefill  B=8, H=32, n=8192 tokens, chunk 64, from an empty state;
+  decode   1024 steps for every (b, h), continuing from the prefill state.
+One step = one prefill over the batch plus the 1024 decode steps.  Inputs are
+seeded synthetic N(0,1) tensors resident in HBM before timing starts.
+
+Prints ONE JSON line.  `value` is whole-job tokens/s: (B*n + B*decode_steps)
+tokens per step divided by the step time; the prefill and decode rates are
+reported separately next to it.  `roofline` is for the kernel that takes the
+largest share of the step (`rooflines` lists both); its achieved rate is the
+algorithmic work of one launch divided by the launch's average duration,
+measured with HIP events on the stream the kernels run on.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--decode-steps M] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+
+WORKLOAD_ID = 3
+B, H, N, DK, DV, P, CHUNK = 8, 32, 8192, 32, 32, 4, 64
+
+
+def feature_count(d, p):
+    return math.comb(d + p - 1, p - 1)
+
+
+def prefill_flops_per_head_token(dk, dv, P, C):
+    """Algorithmic prefill work per head-token: the two state contractions,
+    readout phi(Q_c) S and update phi(K_c)^T [V_c|1], 2*D*(d_v+1) each, plus the
+    causal intra-chunk term, on average (C+1)/2 keys per query times
+    2*d_k (scores) + 2*(d_v+1) (weights times [v|1])."""
+    D = feature_count(dk, P)
+    return 4 * D * (dv + 1) + (C + 1) * (dk + dv + 1)
+
+
+def decode_bytes_per_head_step(dk, dv, P, elem_bytes):
+    """Algorithmic decode traffic per head-step: read and write the float32
+    state once, D*(d_v+1)*8 bytes, plus q, k, v in and y out."""
+    D = feature_count(dk, P)
+    return 8 * D * (dv + 1) + elem_bytes * (2 * dk + 2 * dv)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--decode-steps", type=int, default=1024)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-heads", type=int, default=2)
+    return ap.parse_args()
+
+
+def make_inputs(dec_steps):
+    import numpy as np
+    import torch
+
+    import sata_synth as syn
+    n_tot = N + dec_steps
+    q = np.empty((B, H, n_tot, DK), np.float32)
+    k = np.empty((B, H, n_tot, DK), np.float32)
+    v = np.empty((B, H, n_tot, DV), np.float32)
+    for b in range(B):
+        for h in range(H):
+            q[b, h], k[b, h], v[b, h] = syn.make_head(WORKLOAD_ID, b, h, n_tot, DK, DV, "bf16")
+    dev = torch.device("cuda:0")
+
+    def up(a):
+        return torch.from_numpy(a).to(dev).to(torch.bfloat16)
+
+    pre = [up(np.ascontiguousarray(a[:, :, :N])) for a in (q, k, v)]
+    # decode inputs laid out [step][B][H][d] so every step reads a contiguous slice
+    dec = [up(np.ascontiguousarray(a[:, :, N:].transpose(2, 0, 1, 3))) for a in (q, k, v)]
+    return pre, dec
+
+
+def cpu_baseline(n_heads, dec_rows):
+    """Times the float64 oracle on a bounded sample of the same workload."""
+    import numpy as np
+
+    import oracle
+    import sata_synth as syn
+    threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    heads = [(0, 0), (B - 1, H - 1), (3, 17), (5, 9)][:n_heads]
+    t_pre = t_dec = 0.0
+    for b, h in heads:
+        q, k, v = syn.make_head(WORKLOAD_ID, b, h, N + dec_rows, DK, DV, "bf16")
+        t0 = time.perf_counter()
+        oracle.taylor_attention(q[:N], k[:N], v[:N], P)
+        t1 = time.perf_counter()
+        oracle.taylor_attention_rows(q, k, v, P, list(range(N, N + dec_rows)))
+        t2 = time.perf_counter()
+        t_pre += t1 - t0
+        t_dec += t2 - t1
+    # seconds per head-token, scaled to tokens of the whole batch (H heads per token)
+    pre_tok_s = (len(heads) * N) / t_pre / H
+    dec_tok_s = (len(heads) * dec_rows) / t_dec / H
+    return {
+        "value": None, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+        "prefill_tokens_per_s": pre_tok_s, "decode_tokens_per_s": dec_tok_s,
+        "sample": (f"{len(heads)} of {B * H} heads: full {N}-token causal prefill by the direct "
+                   f"float64 definition, plus {dec_rows} decode rows at positions {N}..{N + dec_rows - 1}; "
+                   f"rates scaled to whole-batch tokens (1 token = {H} head-tokens); decode rows near "
+                   f"position {N} stand in for all {B}x{H} decode rows"),
+        "seconds": t_pre + t_dec,
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(heads shard across GPUs with no exchange, so per-GPU throughput is the N=1 figure)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2602_00294_amd as sata
+    sata.load_library()
+    assert torch.cuda.is_available(), "no GPU"
+
+    pre, dec = make_inputs(args.decode_steps)
+    D = feature_count(DK, P)
+    y = torch.empty(B, H, N, DV, dtype=torch.bfloat16, device="cuda")
+    S = torch.empty(B, H, D, DV + 1, dtype=torch.float32, device="cuda")
+    ydec = torch.empty(args.decode_steps, B, H, DV, dtype=torch.bfloat16, device="cuda")
+
+    def one_step(ev=None):
+        if ev:
+            ev[0].record()
+        sata.prefill(*pre, P, CHUNK, y=y, S=S)
+        if ev:
+            ev[1].record()
+        for t in range(args.decode_steps):
+            sata.decode_step(S, dec[0][t], dec[1][t], dec[2][t], P, y=ydec[t])
+        if ev:
+            ev[2].record()
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        one_step(events[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    pre_ms = sum(e[0].elapsed_time(e[1]) for e in events) / args.steps
+    dec_ms = sum(e[1].elapsed_time(e[2]) for e in events) / args.steps
+    step_ms = wall * 1e3 / args.steps
+    tokens = B * N + B * args.decode_steps
+    value = tokens / (step_ms * 1e-3)
+    pre_tok_s = B * N / (pre_ms * 1e-3)
+    dec_tok_s = B * args.decode_steps / (dec_ms * 1e-3)
+
+    pre_flops = prefill_flops_per_head_token(DK, DV, P, CHUNK) * B * H * N
+    pre_ach = pre_flops / (pre_ms * 1e-3) / 1e12
+    dec_bytes = decode_bytes_per_head_step(DK, DV, P, 2) * B * H
+    dec_ach = dec_bytes / (dec_ms * 1e-3 / args.decode_steps) / 1e9
+    roof_pre = {"kernel": "sata_prefill (all launches of one call)", "bound": "mfma",
+                "achieved": pre_ach, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": pre_ach / PEAK_BF16_TFLOPS, "traffic": None,
+                "work_per_launch": pre_flops}
+    roof_dec = {"kernel": "sata_decode_step (all launches of one call)", "bound": "hbm",
+                "achieved": dec_ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": dec_ach / PEAK_HBM_GBS, "traffic": None,
+                "work_per_launch": dec_bytes}
+    dominant = roof_pre if pre_ms >= dec_ms else roof_dec
+
+    # parity spot check of what was just timed: first and last head, a few rows
+    import numpy as np
+
+    import oracle
+    import sata_synth as syn
+    torch.cuda.synchronize()
+    parity = {}
+    yh = y.float().cpu().numpy()
+    for (b, h) in ((0, 0), (B - 1, H - 1)):
+        q, k, v = syn.make_head(WORKLOAD_ID, b, h, N, DK, DV, "bf16")
+        rows = [0, 63, 64, 4095, N - 1]
+        yr, _, kap = oracle.taylor_attention_rows(q, k, v, P, rows)
+        err, _ = oracle.max_row_rel_error(yh[b, h, rows], yr, kap)
+        parity[f"b{b}h{h}"] = err
+
+    line = {
+        "metric": "prefill tokens/s + decode tokens/s (d_k=32,P=4); % MFMA/HBM roofline",
+        "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": step_ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": (f"causal prefill B={B} H={H} n={N} d_k=d_v={DK} P={P} (D={D}) bf16 chunk={CHUNK} "
+                                f"then {args.decode_steps} decode steps"),
+                   "global_batch": B, "seq_len": N, "decode_steps": args.decode_steps, "heads": H,
+                   "d_k": DK, "d_v": DV, "P": P, "chunk": CHUNK, "parallelism": "single GPU"},
+        "prefill_tokens_per_s": pre_tok_s, "decode_tokens_per_s": dec_tok_s,
+        "prefill_ms": pre_ms, "decode_ms_per_step": dec_ms / args.decode_steps,
+        "roofline": dominant, "rooflines": {"prefill": roof_pre, "decode": roof_dec},
+        "parity_max_row_rel_err": parity,
+    }
+    if not args.no_cpu_baseline:
+        cb = cpu_baseline(args.cpu_sample_heads, 64)
+        whole = tokens / (B * N / cb["prefill_tokens_per_s"] + B * args.decode_steps / cb["decode_tokens_per_s"])
+        cb["value"] = whole
+        line["cpu_baseline"] = cb
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,4 +1,4 @@
-// Matrix-core (MFMA) prefill for bfloat16 inputs.
+// Matrix-core (MFMA) prefill for bfloat16 inputs, P = 4.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -8,6 +8,9 @@
 namespace sata {
 
 struct MfmaPrefillPlan {
+  int dk = 0, dv = 0;
+  int nslices = 0;        // workgroups per head
+  size_t partial_bytes = 0;
   size_t workspace_bytes = 0;
 };
 

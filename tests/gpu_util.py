@@ -27,6 +27,9 @@ def check_prefill_head(y_gpu, S_gpu, q, k, v, P, dtype, label=""):
 
     Returns (max row error, excluded rows, state error or None)."""
     y_ref, _, kappa = oracle.taylor_attention(q, k, v, P)
+    # rows whose denominator cancels (kappa > KAPPA_MAX, even P only) may divide by
+    # a rounded zero; every other row must be finite and within tolerance
+    assert np.all(np.isfinite(y_gpu[kappa <= KAPPA_MAX])), f"{label}: non-finite well-conditioned row"
     err, excluded = max_row_rel_error(y_gpu, y_ref, kappa)
     assert err <= TOL[dtype], f"{label}: max row rel error {err:.3e} > {TOL[dtype]:.0e} (excluded {excluded})"
     s_err = None
