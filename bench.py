@@ -62,7 +62,11 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--decode-steps", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-heads", type=int, default=2)
+    ap.add_argument("--cpu-sample-heads", type=int, default=24)
+    ap.add_argument("--cpu-sample-decode-rows", type=int, default=128)
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="before timing, run one device-to-device copy of this many MiB (a kernel of "
+                         "known traffic for calibrating hardware byte counters)")
     return ap.parse_args()
 
 
@@ -96,7 +100,10 @@ def cpu_baseline(n_heads, dec_rows):
     import oracle
     import sata_synth as syn
     threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
-    heads = [(0, 0), (B - 1, H - 1), (3, 17), (5, 9)][:n_heads]
+    rng = np.random.default_rng(7)
+    heads = [(0, 0), (B - 1, H - 1)] + [(int(b), int(h)) for b, h in
+                                         zip(rng.integers(0, B, n_heads), rng.integers(0, H, n_heads))]
+    heads = heads[:n_heads]
     t_pre = t_dec = 0.0
     for b, h in heads:
         q, k, v = syn.make_head(WORKLOAD_ID, b, h, N + dec_rows, DK, DV, "bf16")
@@ -136,6 +143,12 @@ def main():
     assert torch.cuda.is_available(), "no GPU"
 
     pre, dec = make_inputs(args.decode_steps)
+    if args.copy_probe_mib > 0:
+        src = torch.ones(args.copy_probe_mib << 18, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     D = feature_count(DK, P)
     y = torch.empty(B, H, N, DV, dtype=torch.bfloat16, device="cuda")
     S = torch.empty(B, H, D, DV + 1, dtype=torch.float32, device="cuda")
@@ -216,7 +229,7 @@ def main():
         "parity_max_row_rel_err": parity,
     }
     if not args.no_cpu_baseline:
-        cb = cpu_baseline(args.cpu_sample_heads, 64)
+        cb = cpu_baseline(args.cpu_sample_heads, args.cpu_sample_decode_rows)
         whole = tokens / (B * N / cb["prefill_tokens_per_s"] + B * args.decode_steps / cb["decode_tokens_per_s"])
         cb["value"] = whole
         line["cpu_baseline"] = cb

@@ -22,8 +22,8 @@ hipError_t launch_feature_map(const void* x, bool bf16, int64_t rows, const DevT
 // ---- decode step -------------------------------------------------------------
 struct DecodePlan {
   int fps = 0;      // features per workgroup slice
-  int nslices = 0;  // slices per head
-  size_t partial_bytes = 0;
+  int nslices = 0;  // slices per head (1: one workgroup streams the whole head)
+  int threads = 0;  // workgroup size
 };
 DecodePlan plan_decode(int64_t D, int dv);
 hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, void* y, bool bf16,

@@ -46,48 +46,40 @@ feature_map_kernel(const T* __restrict__ x, int64_t rows, int d, const uint64_t*
 }
 
 // ---------------------------------------------------------------- decode step
-//
-// Workgroup (slice s, head bh) owns features [s*fps, min(D, (s+1)*fps)).  It
-// builds phi(q) and phi(k) for them in LDS, then streams its rows of S once:
-// thread t < R*E (R = rows per pass) handles column j = t % E of row t / E, so
-// consecutive threads touch consecutive addresses; each element is updated
-// (S += phi_k[f] * [v|1][j]) and immediately read out (o_j += phi_q[f] * S).
 
-template <typename T>
-__global__ void __launch_bounds__(kThreads)
-decode_main_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __restrict__ k,
-                   const T* __restrict__ v, T* __restrict__ y, float* __restrict__ partial,
-                   const uint64_t* __restrict__ packed, const float* __restrict__ weight, int64_t D,
-                   int dk, int dv, int fps, int nslices) {
-  extern __shared__ float lds[];
+// Whole-head decode: one workgroup streams all rows of one head's state, so
+// the readout needs no cross-workgroup reduction.  Thread t < R*E (R = rows
+// per pass) owns column j = t % E of rows t / E + k*R: consecutive threads
+// touch consecutive addresses, each element is updated (S += phi_k[f] * [v|1][j])
+// and immediately read out (o_j += phi_q[f] * S).  Large heads are split over
+// several workgroups instead (decode_slice_kernel + decode_finalize_kernel).
+template <typename T, int NTH>
+__device__ __forceinline__ void decode_rows(float* __restrict__ S, const T* __restrict__ q,
+                                            const T* __restrict__ k, const T* __restrict__ v,
+                                            const uint64_t* __restrict__ packed, const float* __restrict__ weight,
+                                            int64_t D, int dk, int dv, int64_t bh, int64_t f0, int nf, float* lds) {
   const int E = dv + 1;
   float* xq = lds;               // [dk]
   float* xk = xq + dk;           // [dk]
   float* ve = xk + dk;           // [E]
-  float* fq = ve + E;            // [fps]
-  float* fk = fq + fps;          // [fps]
-  float* red = fk + fps;         // [kThreads]
-  const int s = blockIdx.x;
-  const int64_t bh = blockIdx.y;
+  float* fq = ve + E;            // [nf]
+  float* fk = fq + nf;           // [nf]
+  float* red = fk + nf;          // [NTH]
   const int tid = threadIdx.x;
-  const int64_t f0 = (int64_t)s * fps;
-  const int nf = (int)min<int64_t>(fps, D - f0);
-
-  for (int i = tid; i < dk; i += kThreads) {
+  for (int i = tid; i < dk; i += NTH) {
     xq[i] = to_f32(q[bh * dk + i]);
     xk[i] = to_f32(k[bh * dk + i]);
   }
-  for (int i = tid; i < E; i += kThreads) ve[i] = (i < dv) ? to_f32(v[bh * dv + i]) : 1.0f;
+  for (int i = tid; i < E; i += NTH) ve[i] = (i < dv) ? to_f32(v[bh * dv + i]) : 1.0f;
   __syncthreads();
-  for (int f = tid; f < nf; f += kThreads) {
+  for (int f = tid; f < nf; f += NTH) {
     const uint64_t pk = packed[f0 + f];
     const float w = weight[f0 + f];
     fq[f] = feature_value(pk, w, xq);
     fk[f] = feature_value(pk, w, xk);
   }
   __syncthreads();
-
-  const int R = kThreads / E;  // rows per pass
+  const int R = NTH / E;  // rows per pass
   float acc = 0.0f;
   if (tid < R * E) {
     const int r = tid / E;
@@ -95,27 +87,21 @@ decode_main_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
     const float vj = ve[j];
     float* base = S + (bh * D + f0) * E + j;
     int f = r;
-    // four rows in flight per thread
-    for (; f + 3 * R < nf; f += 4 * R) {
-      float s0 = base[(int64_t)f * E];
-      float s1 = base[(int64_t)(f + R) * E];
-      float s2 = base[(int64_t)(f + 2 * R) * E];
-      float s3 = base[(int64_t)(f + 3 * R) * E];
-      s0 += fk[f] * vj;
-      s1 += fk[f + R] * vj;
-      s2 += fk[f + 2 * R] * vj;
-      s3 += fk[f + 3 * R] * vj;
-      base[(int64_t)f * E] = s0;
-      base[(int64_t)(f + R) * E] = s1;
-      base[(int64_t)(f + 2 * R) * E] = s2;
-      base[(int64_t)(f + 3 * R) * E] = s3;
-      acc += fq[f] * s0;
-      acc += fq[f + R] * s1;
-      acc += fq[f + 2 * R] * s2;
-      acc += fq[f + 3 * R] * s3;
+    // eight rows in flight per thread
+    for (; f + 7 * R < nf; f += 8 * R) {
+      float x[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) x[u] = base[(int64_t)(f + u * R) * E];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        x[u] += fk[f + u * R] * vj;
+        base[(int64_t)(f + u * R) * E] = x[u];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc += fq[f + u * R] * x[u];
     }
     for (; f < nf; f += R) {
-      float s0 = base[(int64_t)f * E] + fk[f] * vj;
+      const float s0 = base[(int64_t)f * E] + fk[f] * vj;
       base[(int64_t)f * E] = s0;
       acc += fq[f] * s0;
     }
@@ -128,11 +114,33 @@ decode_main_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
     red[tid] = o;  // only this thread reads red[r*E + tid] for its own column
   }
   __syncthreads();
-  if (nslices == 1) {
-    if (tid < dv) y[bh * dv + tid] = from_f32<T>(red[tid] / red[dv]);
-  } else if (tid < E) {
-    partial[(bh * nslices + s) * E + tid] = red[tid];
-  }
+}
+
+template <typename T, int NTH>
+__global__ void __launch_bounds__(NTH)
+decode_head_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __restrict__ k,
+                   const T* __restrict__ v, T* __restrict__ y, const uint64_t* __restrict__ packed,
+                   const float* __restrict__ weight, int64_t D, int dk, int dv) {
+  extern __shared__ float lds[];
+  const int64_t bh = blockIdx.x;
+  decode_rows<T, NTH>(S, q, k, v, packed, weight, D, dk, dv, bh, 0, (int)D, lds);
+  const float* red = lds + 2 * dk + (dv + 1) + 2 * D;
+  for (int j = threadIdx.x; j < dv; j += NTH) y[bh * dv + j] = from_f32<T>(red[j] / red[dv]);
+}
+
+template <typename T>
+__global__ void __launch_bounds__(kThreads)
+decode_slice_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __restrict__ k,
+                    const T* __restrict__ v, float* __restrict__ partial, const uint64_t* __restrict__ packed,
+                    const float* __restrict__ weight, int64_t D, int dk, int dv, int fps, int nslices) {
+  extern __shared__ float lds[];
+  const int s = blockIdx.x;
+  const int64_t bh = blockIdx.y;
+  const int64_t f0 = (int64_t)s * fps;
+  const int nf = (int)min<int64_t>(fps, D - f0);
+  decode_rows<T, kThreads>(S, q, k, v, packed, weight, D, dk, dv, bh, f0, nf, lds);
+  const float* red = lds + 2 * dk + (dv + 1) + 2 * nf;
+  for (int j = threadIdx.x; j < dv + 1; j += kThreads) partial[(bh * nslices + s) * (dv + 1) + j] = red[j];
 }
 
 template <typename T>
@@ -337,13 +345,21 @@ hipError_t launch_feature_map(const void* x, bool bf16, int64_t rows, const DevT
 DecodePlan plan_decode(int64_t D, int dv) {
   const int E = dv + 1;
   DecodePlan p;
-  // about 32K state elements (128 KB of float32) per workgroup
+  // A head whose feature values fit in LDS next to nothing else is streamed by
+  // one workgroup (no cross-workgroup reduction, one launch per step).
+  if (2 * D * (int64_t)sizeof(float) <= 96 * 1024) {
+    p.fps = (int)D;
+    p.nslices = 1;
+    p.threads = D * E > 65536 ? 1024 : 256;
+    return p;
+  }
+  // Larger heads: about 32K state elements (128 KB of float32) per workgroup.
   int64_t fps = std::max<int64_t>(kThreads / E, (32768 + E - 1) / E);
   fps = std::min<int64_t>(fps, 4096);
   fps = std::min<int64_t>(fps, D);
   p.fps = (int)fps;
   p.nslices = (int)((D + fps - 1) / fps);
-  p.partial_bytes = 0;
+  p.threads = kThreads;
   return p;
 }
 
@@ -351,18 +367,36 @@ hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, 
                          int dk, int dv, const DevTable& t, const DecodePlan& plan, float* partial,
                          hipStream_t s) {
   const int E = dv + 1;
+  if (plan.nslices == 1) {
+    // whole head per workgroup: one launch per step
+    const size_t lds = sizeof(float) * (2 * dk + E + 2 * (size_t)t.D + plan.threads);
+    hipError_t e;
+#define SATA_DECODE_HEAD(TT, NTH)                                                                         \
+  e = hipFuncSetAttribute((const void*)decode_head_kernel<TT, NTH>, hipFuncAttributeMaxDynamicSharedMemorySize, \
+                          (int)lds);                                                                      \
+  if (e != hipSuccess) return e;                                                                          \
+  hipLaunchKernelGGL((decode_head_kernel<TT, NTH>), dim3((unsigned)BH), dim3(NTH), lds, s, S, (const TT*)q,  \
+                     (const TT*)k, (const TT*)v, (TT*)y, t.packed, t.weight, t.D, dk, dv)
+    if (plan.threads == 1024) {
+      if (bf16) { SATA_DECODE_HEAD(bf16_t, 1024); } else { SATA_DECODE_HEAD(float, 1024); }
+    } else {
+      if (bf16) { SATA_DECODE_HEAD(bf16_t, 256); } else { SATA_DECODE_HEAD(float, 256); }
+    }
+#undef SATA_DECODE_HEAD
+    return hipGetLastError();
+  }
   const size_t lds = sizeof(float) * (2 * dk + E + 2 * plan.fps + kThreads);
   dim3 grid((unsigned)plan.nslices, (unsigned)BH);
   if (bf16)
-    hipLaunchKernelGGL(decode_main_kernel<bf16_t>, grid, dim3(kThreads), lds, s, S, (const bf16_t*)q,
-                       (const bf16_t*)k, (const bf16_t*)v, (bf16_t*)y, partial, t.packed, t.weight, t.D, dk,
-                       dv, plan.fps, plan.nslices);
+    hipLaunchKernelGGL(decode_slice_kernel<bf16_t>, grid, dim3(kThreads), lds, s, S, (const bf16_t*)q,
+                       (const bf16_t*)k, (const bf16_t*)v, partial, t.packed, t.weight, t.D, dk, dv, plan.fps,
+                       plan.nslices);
   else
-    hipLaunchKernelGGL(decode_main_kernel<float>, grid, dim3(kThreads), lds, s, S, (const float*)q,
-                       (const float*)k, (const float*)v, (float*)y, partial, t.packed, t.weight, t.D, dk, dv,
-                       plan.fps, plan.nslices);
+    hipLaunchKernelGGL(decode_slice_kernel<float>, grid, dim3(kThreads), lds, s, S, (const float*)q,
+                       (const float*)k, (const float*)v, partial, t.packed, t.weight, t.D, dk, dv, plan.fps,
+                       plan.nslices);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || plan.nslices == 1) return e;
+  if (e != hipSuccess) return e;
   const size_t lds2 = sizeof(float) * E;
   if (bf16)
     hipLaunchKernelGGL(decode_finalize_kernel<bf16_t>, dim3((unsigned)BH), dim3(64), lds2, s, partial,
@@ -373,7 +407,8 @@ hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, 
   return hipGetLastError();
 }
 
-static constexpr size_t kLdsBudget = 64 * 1024;
+// gfx950 offers 160 KB of LDS per workgroup; the generic kernels use up to 128 KB.
+static constexpr size_t kLdsBudget = 128 * 1024;
 
 bool plan_prefill_generic(int64_t D, int BH, int n, int dk, int dv, int chunk, size_t max_ws_bytes,
                           PrefillGenericPlan* plan) {
@@ -407,6 +442,21 @@ hipError_t launch_prefill_generic(const void* q, const void* k, const void* v, v
                                   const PrefillGenericPlan& plan, float* S_state, float* partial,
                                   hipStream_t s) {
   const int C = chunk;
+  hipError_t ea;
+  if (bf16) {
+    ea = hipFuncSetAttribute((const void*)prefill_generic_main<bf16_t>,
+                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)plan.lds_main);
+    if (ea == hipSuccess)
+      ea = hipFuncSetAttribute((const void*)prefill_generic_finalize<bf16_t>,
+                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)plan.lds_final);
+  } else {
+    ea = hipFuncSetAttribute((const void*)prefill_generic_main<float>,
+                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)plan.lds_main);
+    if (ea == hipSuccess)
+      ea = hipFuncSetAttribute((const void*)prefill_generic_finalize<float>,
+                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)plan.lds_final);
+  }
+  if (ea != hipSuccess) return ea;
   for (int seg0 = 0; seg0 < n; seg0 += plan.seg_len) {
     const int first = seg0 == 0 ? 1 : 0;
     dim3 g1((unsigned)plan.nslices, (unsigned)BH);

@@ -143,9 +143,9 @@ __device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// Phi(Q) generation for this lane's token row: groups J, J+NW, J+2NW, ... of 8
-// columns, up to the slice's need (group indices are compile-time constants,
-// so every coordinate index below is a register, not a memory lookup).
+// Feature generation for this lane's token row: groups J, J+NW, J+2NW, ... of
+// 8 LDS columns up to the slice's need.  Group indices are compile-time
+// constants, so every coordinate index below is a register.
 template <int DK, int NW, int J>
 __device__ __forceinline__ void gen_q_from(const float (&xt)[DK], char* row, int ngneed) {
   if constexpr (J < Geo<DK>::NG) {
@@ -155,12 +155,11 @@ __device__ __forceinline__ void gen_q_from(const float (&xt)[DK], char* row, int
     w.y = pack2(col_value<DK, 8 * J + 2>(xt), col_value<DK, 8 * J + 3>(xt));
     w.z = pack2(col_value<DK, 8 * J + 4>(xt), col_value<DK, 8 * J + 5>(xt));
     w.w = pack2(col_value<DK, 8 * J + 6>(xt), col_value<DK, 8 * J + 7>(xt));
-    *(uint4*)(row + 16 * J) = w;
+    *(uint4*)(row + 16 * J) = w;  // Phi(Q): [token][column]
     gen_q_from<DK, NW, J + NW>(xt, row, ngneed);
   }
 }
 
-// Phi(K) generation into the transposed [feature][token] layout.
 template <int DK, int NW, int J>
 __device__ __forceinline__ void gen_k_from(const float (&xt)[DK], char* col, int ngneed) {
   if constexpr (J < Geo<DK>::NG) {
@@ -170,7 +169,7 @@ __device__ __forceinline__ void gen_k_from(const float (&xt)[DK], char* col, int
     const uint32_t w1 = pack2(col_value<DK, 8 * J + 2>(xt), col_value<DK, 8 * J + 3>(xt));
     const uint32_t w2 = pack2(col_value<DK, 8 * J + 4>(xt), col_value<DK, 8 * J + 5>(xt));
     const uint32_t w3 = pack2(col_value<DK, 8 * J + 6>(xt), col_value<DK, 8 * J + 7>(xt));
-    char* p = col + (8 * J) * KS;
+    char* p = col + (8 * J) * KS;  // Phi(K): [column][token]
     *(u16*)(p + 0 * KS) = (u16)w0;
     *(u16*)(p + 1 * KS) = (u16)(w0 >> 16);
     *(u16*)(p + 2 * KS) = (u16)w1;
@@ -239,7 +238,9 @@ struct TileFetch {
 template <int DK, int DV, int NW, int PPW>
 struct MainLds {
   static constexpr int kColMeta = 0;
-  static constexpr int kPhi = kColMeta + Geo<DK>::LW * 4;
+  static constexpr int kZFac = kColMeta + Geo<DK>::LW * 4;   // normaliser row factor 3/(deg+1)
+  static constexpr int kRFac = kZFac + Geo<DK>::LW * 4;      // 1/c1 for rows with first(g) == i1
+  static constexpr int kPhi = kRFac + Geo<DK>::LW * 4;
   static constexpr int kPhiBytes = (kGroup * Geo<DK>::QS > Geo<DK>::LW * Geo<DK>::KS)
                                        ? kGroup * Geo<DK>::QS
                                        : Geo<DK>::LW * Geo<DK>::KS;
@@ -260,13 +261,6 @@ __device__ __forceinline__ int pk_i1(uint32_t x) { return (x >> 12) & 255; }
 __device__ __forceinline__ int pk_nrows(uint32_t x) { return (x >> 20) & 63; }
 __device__ __forceinline__ int pk_rho_from(uint32_t x) { return (x >> 26) & 63; }
 
-// Normaliser rows carry a factor 1/(deg(g)+1); 1/(P-1) = 1/3 for every degree-2
-// row is folded into the update operand, the rest is applied per row here.
-__device__ __forceinline__ float zmat_row_factor(uint32_t cm) {
-  const int deg = (cm >> 16) & 0xff;
-  return deg == 0xff ? 0.0f : 3.0f / (float)(deg + 1);
-}
-
 template <int DK, int DV, int NW, int PPW>
 __global__ void __launch_bounds__(NW * 64)
 prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u16* __restrict__ v,
@@ -283,6 +277,8 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
 
   extern __shared__ __attribute__((aligned(16))) char smem[];
   uint32_t* colmeta = (uint32_t*)(smem + L::kColMeta);
+  float* zfac = (float*)(smem + L::kZFac);
+  float* rfac = (float*)(smem + L::kRFac);
   char* phi = smem + L::kPhi;
   float* qT = (float*)(smem + L::kQT);
   float* kT = (float*)(smem + L::kKT);
@@ -299,7 +295,14 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
   const int ngneed = slice_ng[slice];
   const float xscale = 1.0f / sqrtf(sqrtf((float)DK));  // d^(-1/4)
 
-  for (int i = tid; i < G::LW; i += NTH) colmeta[i] = colmeta_g[i];
+  for (int i = tid; i < G::LW; i += NTH) {
+    const uint32_t cm = colmeta_g[i];
+    colmeta[i] = cm;
+    const int deg = (cm >> 16) & 0xff;
+    // the normaliser's 1/(deg+1) relative to the 1/3 folded into its update
+    zfac[i] = deg == 2 ? 1.0f : deg == 1 ? 1.5f : deg == 0 ? 3.0f : 0.0f;
+    rfac[i] = ((cm >> 8) & 0xff) == 2 ? (1.0f / 3.0f) : 0.5f;  // 1/(1 + count of first index)
+  }
   // constant factor rows after the coordinates: row DK = 1 (low pairs),
   // row DK+1 = 1/3 (normaliser pairs, the factor 1/(P-1) of degree-2 rows)
   for (int i = tid; i < kGroup; i += NTH) {
@@ -362,8 +365,9 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
       }
       __syncthreads();
       for (int h = 0; h * 32 < ntok; ++h) {
-        // R accumulates a run of one top block, or (in waves that own the
-        // normaliser pairs) the normaliser readout; the planner never mixes the two
+        // Readout of 32 tokens (two row tiles) against S_{c-1}.  R accumulates a
+        // run of one block (or, in waves that own the normaliser pairs, the
+        // normaliser readout; the planner never mixes the two).
         f32x4 O[2][NT], R[2][NT];
         float zp[2][4];
 #pragma unroll
@@ -390,26 +394,21 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
             const uint2 hi = *(const uint2*)(p + 32);
             a[m] = __builtin_bit_cast(bf16x8, uint4{lo.x, lo.y, hi.x, hi.y});
           }
-          float fac[8];
-#pragma unroll
-          for (int i = 0; i < 8; ++i) fac[i] = 1.0f;
-          if (pk_rowfac(x)) {
-            const int kind = pk_kind(x);
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-              const int r = i < 4 ? 4 * g4 + i : 16 + 4 * g4 + i - 4;
-              const uint32_t cm = colmeta[col0 + r];
-              if (kind == kZmat) fac[i] = zmat_row_factor(cm);
-              else if (r >= pk_rho_from(x)) fac[i] = 1.0f / (float)(1 + ((cm >> 8) & 0xff));
-            }
-          }
+          // Row factors, branch-free: rows r >= `from` take the column's factor
+          // (normaliser pairs at the low-degree boundary: 3/(deg+1); top pairs:
+          // 1/c1 on rows whose g starts with i1), all other rows 1.
+          const bool zk = pk_kind(x) == kZmat;
+          const float* ftab = zk ? zfac : rfac;
+          const int from = pk_rowfac(x) ? (zk ? 0 : pk_rho_from(x)) : 32;
+          const f32x4 f0 = *(const f32x4*)(ftab + col0 + 4 * g4);
+          const f32x4 f1 = *(const f32x4*)(ftab + col0 + 16 + 4 * g4);
 #pragma unroll
           for (int j = 0; j < NT; ++j) {
             float e[8];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              e[i] = S[t][0][j][i] * fac[i];
-              e[4 + i] = S[t][1][j][i] * fac[4 + i];
+              e[i] = S[t][0][j][i] * (4 * g4 + i >= from ? f0[i] : 1.0f);
+              e[4 + i] = S[t][1][j][i] * (16 + 4 * g4 + i >= from ? f1[i] : 1.0f);
             }
             const bf16x8 b = pack8(e);
 #pragma unroll
@@ -418,7 +417,7 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
           // run epilogue: value runs are scaled per token by q~[t][i1] (low runs by
           // the row of ones) and added to O; the normaliser run is reduced into zp
           if (pk_flags(x) & kLastOfRun) {
-            if (pk_kind(x) == kZmat) {
+            if (zk) {
 #pragma unroll
               for (int m = 0; m < 2; ++m)
 #pragma unroll
@@ -441,10 +440,9 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
 #pragma unroll
               for (int j = 0; j < NT; ++j) R[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
           }
-          __builtin_amdgcn_sched_barrier(0);
         }
-        // normaliser of degrees >= 1: zp holds, per lane, sum over this lane's i1
-        // columns of q~[t][i1] * R[t][i1]; finish the sum across the 16 lanes
+        // normaliser of degrees >= 1: zp holds, per lane, the sum over this lane's
+        // i1 columns of q~[t][i1] * R[t][i1]; finish the sum across the 16 lanes
         if (has_z) {
 #pragma unroll
           for (int m = 0; m < 2; ++m)
@@ -536,7 +534,6 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
                             x1[0] * f1[0], x1[1] * f1[1], x1[2] * f1[2], x1[3] * f1[3]};
               B[ks][j] = pack8(e);
             }
-            __builtin_amdgcn_sched_barrier(0);
           }
         }
         const int col0 = pk_col0(x);
@@ -548,13 +545,12 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
           for (int ks = 0; ks < 2; ++ks) {
             if (ks >= nks) break;
             uint4 w = *(const uint4*)(phi + (col0 + row) * G::KS + (32 * ks + 8 * g4) * 2);
-            if (row >= nrows) w = uint4{0u, 0u, 0u, 0u};
+            if (nrows < 32 && row >= nrows) w = uint4{0u, 0u, 0u, 0u};
             const bf16x8 a = __builtin_bit_cast(bf16x8, w);
 #pragma unroll
             for (int j = 0; j < NT; ++j) S[t][r][j] = mfma(a, B[ks][j], S[t][r][j]);
           }
         }
-        __builtin_amdgcn_sched_barrier(0);
       }
     }
   }

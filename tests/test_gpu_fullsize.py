@@ -1,0 +1,143 @@
+"""GPU parity at the full workload sizes, in the launch configurations the
+benchmark times, checked on sampled outputs the oracle computes one by one.
+
+* d_k = d_v = 32, P = 4, bf16: B=8, H=32, n=8192, chunk 64, then decode steps
+  (the benchmark's workload; same input streams).
+* d_k = d_v = 16, P = 4, bf16: B=64, H=32 (2048 heads), a 2048-token prefill
+  then decode steps.
+* d_k = d_v = 64, P = 4, bf16: B=2, H=8, n=4096, then decode steps.
+* d_k = d_v = 16, float32, 64 heads, n=65536, P in {2, 4, 6}.
+* d_k = d_v = 8, P = 4, float32: one head, n=256, every row and the state.
+
+Rows compared: the first and last rows of chunks near the start, the middle
+and the end, plus seeded random rows; heads: the first, the last and a
+middle one.  States are compared for two heads (float64 route through the
+oracle's feature map).
+"""
+import sys
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+import sata_synth as syn
+from gpu_util import TOL, to_dev, to_host
+from oracle.metrics import max_row_rel_error, state_rel_error
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def sata():
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    import paper_2602_00294_amd as m
+    m.load_library()
+    return m
+
+
+def _say(msg):
+    print(f"[{time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def _rows(n, seed, extra=16):
+    base = {0, 1, 31, 32, 63, 64, 65, 127, n // 2 - 1, n // 2, n - 65, n - 64, n - 2, n - 1}
+    rng = np.random.default_rng(seed)
+    base |= set(int(x) for x in rng.integers(0, n, extra))
+    return sorted(r for r in base if 0 <= r < n)
+
+
+def _gen(workload, B, H, n_tot, d, dtype):
+    """All heads, generated exactly as the benchmark does (one stream of n_tot tokens per head)."""
+    q = np.empty((B, H, n_tot, d), np.float32)
+    k = np.empty_like(q)
+    v = np.empty_like(q)
+    for b in range(B):
+        for h in range(H):
+            q[b, h], k[b, h], v[b, h] = syn.make_head(workload, b, h, n_tot, d, d, dtype)
+    return q, k, v
+
+
+def _check_rows(y, q, k, v, P, heads, rows, dtype, label):
+    worst = 0.0
+    for (b, h) in heads:
+        yr, _, kap = oracle.taylor_attention_rows(q[b, h], k[b, h], v[b, h], P, rows)
+        err, excluded = max_row_rel_error(y[b, h][rows], yr, kap)
+        assert err <= TOL[dtype], f"{label} b{b} h{h}: {err:.3e} (excluded {excluded})"
+        worst = max(worst, err)
+    return worst
+
+
+def _prefill_then_decode(sata, workload, B, H, n, n_dec, d, P, chunk, dtype, heads, state_heads):
+    _say(f"generate inputs workload={workload} B={B} H={H} n={n}+{n_dec} d={d} {dtype}")
+    q, k, v = _gen(workload, B, H, n + n_dec, d, dtype)
+    dev = lambda a: to_dev(np.ascontiguousarray(a), dtype)
+    _say("prefill")
+    y, S = sata.prefill(dev(q[:, :, :n]), dev(k[:, :, :n]), dev(v[:, :, :n]), P, chunk)
+    torch.cuda.synchronize()
+    yh = to_host(y)
+    _say("check prefill rows")
+    worst = _check_rows(yh, q, k, v, P, heads, _rows(n, workload), dtype, "prefill")
+    Sh = to_host(S)
+    for (b, h) in state_heads:
+        _say(f"check state b{b} h{h}")
+        s_err = state_rel_error(Sh[b, h], oracle.state_ref(k[b, h, :n], v[b, h, :n], P))
+        assert s_err <= TOL[dtype], f"state b{b} h{h}: {s_err:.3e}"
+    del Sh
+    _say(f"decode {n_dec} steps")
+    ys = []
+    for t in range(n, n + n_dec):
+        ys.append(to_host(sata.decode_step(S, dev(q[:, :, t]), dev(k[:, :, t]), dev(v[:, :, t]), P)))
+    torch.cuda.synchronize()
+    for (b, h) in heads:
+        yr, _, kap = oracle.taylor_attention_rows(q[b, h], k[b, h], v[b, h], P, list(range(n, n + n_dec)))
+        got = np.stack([yy[b, h] for yy in ys])
+        err, _ = max_row_rel_error(got, yr, kap)
+        assert err <= TOL[dtype], f"decode b{b} h{h}: {err:.3e}"
+        worst = max(worst, err)
+    _say(f"worst row error {worst:.3e}")
+
+
+def test_headline_d32_prefill_and_decode(sata):
+    """The benchmark's workload: same streams (workload 3, 8192 + decode tokens per head)."""
+    B, H, n, d = 8, 32, 8192, 32
+    _prefill_then_decode(sata, 3, B, H, n, 8, d, 4, 64, "bf16",
+                         heads=[(0, 0), (B - 1, H - 1), (3, 17)], state_heads=[(0, 0), (B - 1, H - 1)])
+
+
+def test_decode_workload_d16(sata):
+    B, H, n, d = 64, 32, 2048, 16
+    _prefill_then_decode(sata, 2, B, H, n, 8, d, 4, 64, "bf16",
+                         heads=[(0, 0), (B - 1, H - 1), (31, 5)], state_heads=[(0, 0), (B - 1, H - 1)])
+
+
+def test_large_head_d64(sata):
+    B, H, n, d = 2, 8, 4096, 64
+    _prefill_then_decode(sata, 4, B, H, n, 4, d, 4, 64, "bf16",
+                         heads=[(0, 0), (B - 1, H - 1)], state_heads=[(1, 7)])
+
+
+@pytest.mark.parametrize("P", [2, 4, 6])
+def test_fp32_length_sweep_d16(sata, P):
+    B, H, n, d = 1, 64, 65536, 16
+    _say(f"generate fp32 sweep inputs P={P}")
+    q, k, v = _gen(5, B, H, n, d, "f32")
+    _say(f"prefill n={n} P={P}")
+    y, _ = sata.prefill(*(to_dev(a, "f32") for a in (q, k, v)), P, 64, want_state=False)
+    torch.cuda.synchronize()
+    worst = _check_rows(to_host(y), q, k, v, P, [(0, 0), (0, H - 1), (0, 21)], _rows(n, 50 + P), "f32",
+                        f"sweep P={P}")
+    _say(f"P={P} worst row error {worst:.3e}")
+
+
+def test_single_head_d8_all_rows(sata):
+    q, k, v = syn.make_qkv(1, 1, 1, 256, 8, 8, "f32")
+    y, S = sata.prefill(*(to_dev(a, "f32") for a in (q, k, v)), 4, 64)
+    torch.cuda.synchronize()
+    yr, _, kap = oracle.taylor_attention(q[0, 0], k[0, 0], v[0, 0], 4)
+    err, _ = max_row_rel_error(to_host(y)[0, 0], yr, kap)
+    assert err <= TOL["f32"]
+    assert state_rel_error(to_host(S)[0, 0], oracle.state_ref(k[0, 0], v[0, 0], 4)) <= TOL["f32"]
