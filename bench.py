@@ -55,6 +55,30 @@ def decode_bytes_per_head_step(dk, dv, P, elem_bytes):
     return 8 * D * (dv + 1) + elem_bytes * (2 * dk + 2 * dv)
 
 
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 summaries.
+
+    Each summary under profiles/ carries a line
+      traffic_record: kernel=<name> source=<file> sha256_16=<hash> bytes_per_launch=<bytes>
+    with calibrated FETCH_SIZE + WRITE_SIZE counts.  The figure holds only for the
+    source it was taken on, so None is returned once that file has changed."""
+    import glob
+    import hashlib
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        for line in open(path):
+            if not line.startswith("traffic_record:"):
+                continue
+            rec = dict(kv.split("=", 1) for kv in line.split()[1:])
+            if rec.get("kernel") != kernel:
+                continue
+            src = os.path.join(ROOT, rec["source"])
+            if not os.path.exists(src):
+                return None
+            digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+            return int(rec["bytes_per_launch"]) if digest == rec["sha256_16"] else None
+    return None
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -62,7 +86,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--decode-steps", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-heads", type=int, default=24)
+    ap.add_argument("--cpu-sample-heads", type=int, default=48)
     ap.add_argument("--cpu-sample-decode-rows", type=int, default=128)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before timing, run one device-to-device copy of this many MiB (a kernel of "
@@ -189,13 +213,15 @@ def main():
     pre_ach = pre_flops / (pre_ms * 1e-3) / 1e12
     dec_bytes = decode_bytes_per_head_step(DK, DV, P, 2) * B * H
     dec_ach = dec_bytes / (dec_ms * 1e-3 / args.decode_steps) / 1e9
+    t_main, t_fin = measured_traffic("prefill_mfma_main"), measured_traffic("prefill_mfma_finalize")
+    pre_traffic = t_main + t_fin if t_main is not None and t_fin is not None else None
     roof_pre = {"kernel": "sata_prefill (all launches of one call)", "bound": "mfma",
                 "achieved": pre_ach, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": pre_ach / PEAK_BF16_TFLOPS, "traffic": None,
+                "frac": pre_ach / PEAK_BF16_TFLOPS, "traffic": pre_traffic,
                 "work_per_launch": pre_flops}
     roof_dec = {"kernel": "sata_decode_step (all launches of one call)", "bound": "hbm",
                 "achieved": dec_ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": dec_ach / PEAK_HBM_GBS, "traffic": None,
+                "frac": dec_ach / PEAK_HBM_GBS, "traffic": measured_traffic("decode_head_kernel"),
                 "work_per_launch": dec_bytes}
     dominant = roof_pre if pre_ms >= dec_ms else roof_dec
 
