@@ -12,6 +12,7 @@
 #include <vector>
 
 #include "kernels.hpp"
+#include "prefill_blocks.hpp"
 #include "prefill_mfma.hpp"
 #include "sata.h"
 #include "table.hpp"
@@ -234,6 +235,13 @@ sata_status sata_prefill(const void* q, const void* k, const void* v, sata_dtype
     if ((st = get_workspace(mp.workspace_bytes, s, &ws)) != SATA_OK) return st;
     e = sata::launch_prefill_mfma(q, k, v, y, S_out, BH, n, d_k, d_v, P, chunk, mp, ws, s);
     if (e != hipSuccess) return hip_fail(e, "prefill (matrix-core) launch");
+    return ok();
+  }
+  if (dt == SATA_BF16 && sata::plan_prefill_blocks(BH, n, d_k, d_v, P, chunk, &mp)) {
+    void* ws = nullptr;
+    if ((st = get_workspace(mp.workspace_bytes, s, &ws)) != SATA_OK) return st;
+    e = sata::launch_prefill_blocks(q, k, v, y, S_out, BH, n, d_k, d_v, P, chunk, mp, ws, s);
+    if (e != hipSuccess) return hip_fail(e, "prefill (matrix-core, per-block) launch");
     return ok();
   }
 
