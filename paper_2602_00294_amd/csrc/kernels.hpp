@@ -24,8 +24,10 @@ struct DecodePlan {
   int fps = 0;      // features per workgroup slice
   int nslices = 0;  // slices per head (1: one workgroup streams the whole head)
   int threads = 0;  // workgroup size
+  int flat_tu = 0;  // > 0: whole-head float4 streaming kernel with this many threads in use
+  size_t flat_lds = 0;
 };
-DecodePlan plan_decode(int64_t D, int dv);
+DecodePlan plan_decode(int64_t D, int dk, int dv);
 hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, void* y, bool bf16,
                          int BH, int dk, int dv, const DevTable& t, const DecodePlan& plan,
                          float* partial, hipStream_t s);

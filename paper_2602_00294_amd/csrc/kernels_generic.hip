@@ -15,6 +15,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <numeric>
 
 #include "device_common.hpp"
 #include "kernels.hpp"
@@ -126,6 +127,139 @@ decode_head_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
   decode_rows<T, NTH>(S, q, k, v, packed, weight, D, dk, dv, bh, 0, (int)D, lds);
   const float* red = lds + 2 * dk + (dv + 1) + 2 * D;
   for (int j = threadIdx.x; j < dv; j += NTH) y[bh * dv + j] = from_f32<T>(red[j] / red[dv]);
+}
+
+// Whole-head decode as one flat float4 stream.  A head's state is D*E
+// contiguous floats (E = d_v + 1).  Of the workgroup's threads, tu (a multiple
+// of E / gcd(E, 4)) take part: thread t owns the float4s g = t + tu*m of the
+// head's 16-byte aligned part, whose first element is a0 < 4.  A step of tu
+// float4s is a whole number of rows, so each of a thread's four lanes keeps
+// one value column j for the whole sweep while its row advances by 4 tu / E.
+// Each element is updated (S += phi_k[f] [v|1][j]) and read out at once
+// (o_j += phi_q[f] S); the per-thread column sums are reduced in a fixed
+// order, and the a0 leading and few trailing elements are done by thread 0,
+// so the result is deterministic.  Loads run two groups of kFlatUnroll
+// float4s ahead of the arithmetic.
+constexpr int kFlatUnroll = 4;
+
+template <typename T, int NTH>
+__global__ void __launch_bounds__(NTH)
+decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __restrict__ k,
+                   const T* __restrict__ v, T* __restrict__ y, const uint64_t* __restrict__ packed,
+                   const float* __restrict__ weight, int64_t D, int dk, int dv, int tu) {
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  const int E = dv + 1;
+  const int tid = threadIdx.x;
+  const int64_t bh = blockIdx.x;
+  const int64_t N = D * E;
+  float* const Sh = S + bh * N;
+  float2* const fkq = (float2*)lds;        // [D] {phi_k, phi_q}
+  float* const xq = (float*)(fkq + D);     // [dk]
+  float* const xk = xq + dk;               // [dk]
+  float* const ve = xk + dk;               // [E]
+  float* const red = ve + E;               // [4 tu] per-thread column sums
+  float* const part = red + 4 * tu;        // [8][E]
+  float* const o = part + 8 * E;           // [E]
+
+  const int a0 = (int)((4 - ((bh * N) & 3)) & 3);
+  const int64_t nv = (N - a0) / 4;         // float4s in the aligned part
+  const float4* const Sv = (const float4*)(Sh + a0);
+  const bool active = tid < tu;
+  // the first loads go out before the features are computed
+  float4 cur[kFlatUnroll];
+#pragma unroll
+  for (int u = 0; u < kFlatUnroll; ++u) {
+    const int64_t g = tid + (int64_t)tu * u;
+    cur[u] = (active && g < nv) ? Sv[g] : float4{0.0f, 0.0f, 0.0f, 0.0f};
+  }
+  for (int i = tid; i < dk; i += NTH) {
+    xq[i] = to_f32(q[bh * dk + i]);
+    xk[i] = to_f32(k[bh * dk + i]);
+  }
+  for (int i = tid; i < E; i += NTH) ve[i] = (i < dv) ? to_f32(v[bh * dv + i]) : 1.0f;
+  __syncthreads();
+  for (int64_t f = tid; f < D; f += NTH) {
+    const uint64_t pk = packed[f];
+    const float w = weight[f];
+    fkq[f] = float2{feature_value(pk, w, xk), feature_value(pk, w, xq)};
+  }
+  __syncthreads();
+
+  // this thread's four lanes: rows f0[c] + rps m, columns jc[c]
+  const int rps = 4 * tu / E;
+  int f0[4];
+  float vj[4], acc[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int e = a0 + 4 * tid + c;
+    f0[c] = e / E;
+    vj[c] = ve[e - f0[c] * E];
+    acc[c] = 0.0f;
+  }
+  float4* const Sw = (float4*)(Sh + a0);
+  if (active) {
+    for (int64_t m0 = 0;; m0 += kFlatUnroll) {
+      float4 nxt[kFlatUnroll];
+#pragma unroll
+      for (int u = 0; u < kFlatUnroll; ++u) {
+        const int64_t g = tid + (int64_t)tu * (m0 + kFlatUnroll + u);
+        nxt[u] = (g < nv) ? Sv[g] : float4{0.0f, 0.0f, 0.0f, 0.0f};
+      }
+      bool more = false;
+#pragma unroll
+      for (int u = 0; u < kFlatUnroll; ++u) {
+        const int64_t m = m0 + u;
+        const int64_t g = tid + (int64_t)tu * m;
+        if (g < nv) {
+          float x[4] = {cur[u].x, cur[u].y, cur[u].z, cur[u].w};
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const float2 fw = fkq[f0[c] + rps * m];
+            x[c] += fw.x * vj[c];
+            acc[c] += fw.y * x[c];
+          }
+          Sw[g] = float4{x[0], x[1], x[2], x[3]};
+          more = true;
+        }
+        cur[u] = nxt[u];
+      }
+      if (!more) break;
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) red[4 * tid + c] = acc[c];
+  }
+  __syncthreads();
+  // column sums: 8 partial sums per column over the entries of that column
+  if (tid < 8 * E) {
+    const int j = tid % E, pp = tid / E;
+    const int p0 = ((j - a0) % E + E) % E;  // red[p] holds column (a0 + p) mod E
+    float a = 0.0f;
+    for (int p = p0 + E * pp; p < 4 * tu; p += 8 * E) a += red[p];
+    part[tid] = a;
+  }
+  __syncthreads();
+  if (tid < E) {
+    float a = 0.0f;
+#pragma unroll
+    for (int pp = 0; pp < 8; ++pp) a += part[pp * E + tid];
+    o[tid] = a;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    // the a0 leading and the trailing elements, in order
+    auto one = [&](int64_t e) {
+      const int64_t f = e / E;
+      const int j = (int)(e - f * E);
+      const float2 fw = fkq[f];
+      const float x = Sh[e] + fw.x * ve[j];
+      Sh[e] = x;
+      o[j] += fw.y * x;
+    };
+    for (int64_t e = 0; e < a0 && e < N; ++e) one(e);
+    for (int64_t e = a0 + 4 * nv; e < N; ++e) one(e);
+  }
+  __syncthreads();
+  for (int j = tid; j < dv; j += NTH) y[bh * dv + j] = from_f32<T>(o[j] / o[dv]);
 }
 
 template <typename T>
@@ -342,7 +476,7 @@ hipError_t launch_feature_map(const void* x, bool bf16, int64_t rows, const DevT
   return hipSuccess;
 }
 
-DecodePlan plan_decode(int64_t D, int dv) {
+DecodePlan plan_decode(int64_t D, int dk, int dv) {
   const int E = dv + 1;
   DecodePlan p;
   // A head whose feature values fit in LDS next to nothing else is streamed by
@@ -351,6 +485,16 @@ DecodePlan plan_decode(int64_t D, int dv) {
     p.fps = (int)D;
     p.nslices = 1;
     p.threads = D * E > 65536 ? 1024 : 256;
+    // Such a head is streamed as flat float4s (decode_flat_kernel) when the
+    // state is 16-byte aligned; the row-wise kernel stays for the others.
+    constexpr int nth = 1024;
+    const int unit = E / std::gcd(E, 4);
+    const int tu = (nth / unit) * unit;
+    const size_t lds = sizeof(float2) * (size_t)D + sizeof(float) * (size_t)(2 * dk + E + 4 * tu + 9 * E);
+    if (tu > 0 && 8 * E <= nth && lds <= 150 * 1024) {
+      p.flat_tu = tu;
+      p.flat_lds = lds;
+    }
     return p;
   }
   // Larger heads: about 32K state elements (128 KB of float32) per workgroup.
@@ -367,6 +511,19 @@ hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, 
                          int dk, int dv, const DevTable& t, const DecodePlan& plan, float* partial,
                          hipStream_t s) {
   const int E = dv + 1;
+  if (plan.flat_tu > 0 && ((uintptr_t)S & 15) == 0) {
+    hipError_t e;
+#define SATA_DECODE_FLAT(TT)                                                                              \
+  e = hipFuncSetAttribute((const void*)decode_flat_kernel<TT, 1024>,                                      \
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)plan.flat_lds);                \
+  if (e != hipSuccess) return e;                                                                          \
+  hipLaunchKernelGGL((decode_flat_kernel<TT, 1024>), dim3((unsigned)BH), dim3(1024), plan.flat_lds, s, S,  \
+                     (const TT*)q, (const TT*)k, (const TT*)v, (TT*)y, t.packed, t.weight, t.D, dk, dv,   \
+                     plan.flat_tu)
+    if (bf16) { SATA_DECODE_FLAT(bf16_t); } else { SATA_DECODE_FLAT(float); }
+#undef SATA_DECODE_FLAT
+    return hipGetLastError();
+  }
   if (plan.nslices == 1) {
     // whole head per workgroup: one launch per step
     const size_t lds = sizeof(float) * (2 * dk + E + 2 * (size_t)t.D + plan.threads);

@@ -272,7 +272,7 @@ sata_status sata_decode_step(float* S, const void* q, const void* k, const void*
   hipStream_t s = (hipStream_t)stream;
   sata::DevTable t;
   if ((st = get_table(d_k, P, s, &t)) != SATA_OK) return st;
-  sata::DecodePlan plan = sata::plan_decode(D, d_v);
+  sata::DecodePlan plan = sata::plan_decode(D, d_k, d_v);
   float* partial = nullptr;
   if (plan.nslices > 1) {
     void* ws = nullptr;
