@@ -137,10 +137,11 @@ decode_head_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
 // one value column j for the whole sweep while its row advances by 4 tu / E.
 // Each element is updated (S += phi_k[f] [v|1][j]) and read out at once
 // (o_j += phi_q[f] S); the per-thread column sums are reduced in a fixed
-// order, and the a0 leading and few trailing elements are done by thread 0,
-// so the result is deterministic.  Loads run two groups of kFlatUnroll
-// float4s ahead of the arithmetic.
-constexpr int kFlatUnroll = 4;
+// order.  The a0 leading and (at most 3) trailing elements are loaded at the
+// start by threads of their own and their readout terms added in element
+// order at the end, so the result is deterministic.  Loads run two groups of
+// kFlatUnroll float4s ahead of the arithmetic.
+constexpr int kFlatUnroll = 2;
 
 template <typename T, int NTH>
 __global__ void __launch_bounds__(NTH)
@@ -160,11 +161,20 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
   float* const red = ve + E;               // [4 tu] per-thread column sums
   float* const part = red + 4 * tu;        // [8][E]
   float* const o = part + 8 * E;           // [E]
+  float* const lo_val = o + E;             // [8] readout terms of the leftover elements
+  int* const lo_col = (int*)(lo_val + 8);  // [8] their columns
 
   const int a0 = (int)((4 - ((bh * N) & 3)) & 3);
   const int64_t nv = (N - a0) / 4;         // float4s in the aligned part
   const float4* const Sv = (const float4*)(Sh + a0);
   const bool active = tid < tu;
+  // leftover elements [0, a0) and [a0 + 4 nv, N): one per thread of the last wave
+  const int nlead = (int)min<int64_t>(a0, N);
+  const int nleft = nlead + (int)(N - (a0 + 4 * nv));
+  const int lt = tid - (NTH - 8);
+  const int64_t le = (lt < nlead) ? lt : a0 + 4 * nv + (lt - nlead);
+  float lx = 0.0f;
+  if (lt >= 0 && lt < nleft) lx = Sh[le];
   // the first loads go out before the features are computed
   float4 cur[kFlatUnroll];
 #pragma unroll
@@ -178,12 +188,32 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
   }
   for (int i = tid; i < E; i += NTH) ve[i] = (i < dv) ? to_f32(v[bh * dv + i]) : 1.0f;
   __syncthreads();
-  for (int64_t f = tid; f < D; f += NTH) {
-    const uint64_t pk = packed[f];
-    const float w = weight[f];
-    fkq[f] = float2{feature_value(pk, w, xk), feature_value(pk, w, xq)};
+  // the table entries of up to 8 features per thread are loaded together
+  for (int64_t fb = tid; fb < D; fb += 8 * NTH) {
+    uint64_t pk[8];
+    float w[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int64_t f = fb + (int64_t)NTH * u;
+      pk[u] = (f < D) ? packed[f] : 0;
+      w[u] = (f < D) ? weight[f] : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int64_t f = fb + (int64_t)NTH * u;
+      if (f < D) fkq[f] = float2{feature_value(pk[u], w[u], xk), feature_value(pk[u], w[u], xq)};
+    }
   }
   __syncthreads();
+  if (lt >= 0 && lt < nleft) {
+    const int64_t f = le / E;
+    const int j = (int)(le - f * E);
+    const float2 fw = fkq[f];
+    lx += fw.x * ve[j];
+    Sh[le] = lx;
+    lo_val[lt] = fw.y * lx;
+    lo_col[lt] = j;
+  }
 
   // this thread's four lanes: rows f0[c] + rps m, columns jc[c]
   const int rps = 4 * tu / E;
@@ -245,19 +275,8 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
     o[tid] = a;
   }
   __syncthreads();
-  if (tid == 0) {
-    // the a0 leading and the trailing elements, in order
-    auto one = [&](int64_t e) {
-      const int64_t f = e / E;
-      const int j = (int)(e - f * E);
-      const float2 fw = fkq[f];
-      const float x = Sh[e] + fw.x * ve[j];
-      Sh[e] = x;
-      o[j] += fw.y * x;
-    };
-    for (int64_t e = 0; e < a0 && e < N; ++e) one(e);
-    for (int64_t e = a0 + 4 * nv; e < N; ++e) one(e);
-  }
+  if (tid == 0)
+    for (int i = 0; i < nleft; ++i) o[lo_col[i]] += lo_val[i];  // leftover terms, in element order
   __syncthreads();
   for (int j = tid; j < dv; j += NTH) y[bh * dv + j] = from_f32<T>(o[j] / o[dv]);
 }
@@ -490,7 +509,7 @@ DecodePlan plan_decode(int64_t D, int dk, int dv) {
     constexpr int nth = 1024;
     const int unit = E / std::gcd(E, 4);
     const int tu = (nth / unit) * unit;
-    const size_t lds = sizeof(float2) * (size_t)D + sizeof(float) * (size_t)(2 * dk + E + 4 * tu + 9 * E);
+    const size_t lds = sizeof(float2) * (size_t)D + sizeof(float) * (size_t)(2 * dk + E + 4 * tu + 9 * E + 16);
     if (tu > 0 && 8 * E <= nth && lds <= 150 * 1024) {
       p.flat_tu = tu;
       p.flat_lds = lds;
