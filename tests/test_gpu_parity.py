@@ -169,3 +169,52 @@ def test_decode_large_state_slices(sata):
         yr, Sr = oracle.decode_ref(S0[0, h], q[0, h, :1], k[0, h, :1], v[0, h, :1], P)
         assert max_row_rel_error(y[0, h][None], yr)[0] < 1e-4
         assert state_rel_error(to_host(S)[0, h], Sr) < 1e-6
+
+
+def _random_state(rng, B, H, D, dv):
+    S0 = rng.standard_normal((B, H, D, dv + 1)).astype(np.float32)
+    S0[..., dv] = np.abs(S0[..., dv]) + 50.0       # a comfortably positive normaliser
+    return S0
+
+
+def test_decode_shapes_interleaved_on_one_stream(sata):
+    """Decode calls of different B*H and d on one stream: the work-queue kernel's
+    counters (shared between calls) must be back at zero after every call."""
+    rng = np.random.default_rng(11)
+    P = 4
+    cases = [(1, 3, 32, "bf16"), (2, 40, 16, "bf16"), (1, 3, 32, "bf16"), (3, 5, 8, "f32"), (2, 40, 16, "bf16")]
+    for i, (B, H, d, dtype) in enumerate(cases):
+        _say(f"interleaved decode {i}: B={B} H={H} d={d} {dtype}")
+        D = oracle.feature_count(d, P)
+        S0 = _random_state(rng, B, H, D, d)
+        q, k, v = syn.make_qkv(50 + i, B, H, 1, d, d, dtype)
+        S = torch.from_numpy(S0).cuda()
+        y = to_host(sata.decode_step(S, to_dev(q[:, :, 0].copy(), dtype), to_dev(k[:, :, 0].copy(), dtype),
+                                     to_dev(v[:, :, 0].copy(), dtype), P))
+        torch.cuda.synchronize()
+        S_host = to_host(S)
+        for b in range(B):
+            for h in range(H):
+                yr, Sr = oracle.decode_ref(S0[b, h], q[b, h, :1], k[b, h, :1], v[b, h, :1], P)
+                assert max_row_rel_error(y[b, h][None], yr)[0] < TOL[dtype], f"case {i} b{b} h{h}"
+                assert state_rel_error(S_host[b, h], Sr) < 1e-6, f"case {i} state b{b} h{h}"
+
+
+def test_decode_unaligned_state(sata):
+    """A state tensor that is not 16-byte aligned takes the row-wise kernel."""
+    rng = np.random.default_rng(12)
+    B, H, d, P = 1, 4, 16, 4
+    D = oracle.feature_count(d, P)
+    S0 = _random_state(rng, B, H, D, d)
+    flat = torch.zeros(S0.size + 1, device="cuda")
+    S = flat[1:].view(S0.shape)                    # offset by one float
+    S.copy_(torch.from_numpy(S0).cuda())
+    assert S.data_ptr() % 16 != 0
+    q, k, v = syn.make_qkv(60, B, H, 1, d, d, "f32")
+    y = to_host(sata.decode_step(S, to_dev(q[:, :, 0].copy(), "f32"), to_dev(k[:, :, 0].copy(), "f32"),
+                                 to_dev(v[:, :, 0].copy(), "f32"), P))
+    torch.cuda.synchronize()
+    for h in range(H):
+        yr, Sr = oracle.decode_ref(S0[0, h], q[0, h, :1], k[0, h, :1], v[0, h, :1], P)
+        assert max_row_rel_error(y[0, h][None], yr)[0] < 1e-4
+        assert state_rel_error(to_host(S)[0, h], Sr) < 1e-6
