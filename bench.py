@@ -221,7 +221,7 @@ def main():
                 "work_per_launch": pre_flops}
     roof_dec = {"kernel": "sata_decode_step (all launches of one call)", "bound": "hbm",
                 "achieved": dec_ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": dec_ach / PEAK_HBM_GBS, "traffic": measured_traffic("decode_head_kernel"),
+                "frac": dec_ach / PEAK_HBM_GBS, "traffic": measured_traffic("decode_flat_kernel"),
                 "work_per_launch": dec_bytes}
     dominant = roof_pre if pre_ms >= dec_ms else roof_dec
 

@@ -265,7 +265,7 @@ __device__ __forceinline__ int pk_rho_from(uint32_t x) { return (x >> 26) & 63; 
 
 template <int DK, int DV, int NW, int PPW>
 __global__ void __launch_bounds__(NW * 64)
-prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u16* __restrict__ v,
+prefill_blocks_main(const u16* __restrict__ q, const u16* __restrict__ k, const u16* __restrict__ v,
                   const uint2* __restrict__ pmeta, const int* __restrict__ slice_ng,
                   const uint32_t* __restrict__ colmeta_g, const int* __restrict__ zmap,
                   float* __restrict__ partial, float* __restrict__ S_out, int BH, int n, int C, int nslices) {
@@ -632,7 +632,7 @@ struct FinLayout {
 
 template <int DK, int DV>
 __global__ void __launch_bounds__(256)
-prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, const u16* __restrict__ v,
+prefill_blocks_finalize(const u16* __restrict__ q, const u16* __restrict__ k, const u16* __restrict__ v,
                       const float* __restrict__ partial, u16* __restrict__ y, int BH, int n, int C, int nslices,
                       int P) {
   constexpr int E = DV + 1;
@@ -959,14 +959,14 @@ template <int DK, int DV, int PPW>
 hipError_t launch_typed(const u16* q, const u16* k, const u16* v, u16* y, float* S_out, int BH, int n, int C,
                         const DeviceTables& dt, float* partial, hipStream_t s) {
   using L = MainLds<DK, DV, kNW, PPW>;
-  auto kmain = prefill_mfma_main<DK, DV, kNW, PPW>;
+  auto kmain = prefill_blocks_main<DK, DV, kNW, PPW>;
   hipError_t e = hipFuncSetAttribute((const void*)kmain, hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kmain, dim3((unsigned)dt.nslices, (unsigned)BH), dim3(kNW * 64), L::kBytes, s, q, k, v,
                      dt.pairs, dt.slice_ng, dt.colmeta, dt.zmap, partial, S_out, BH, n, C, dt.nslices);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const FinLayout F(DK, DV, C);
-  auto kfin = prefill_mfma_finalize<DK, DV>;
+  auto kfin = prefill_blocks_finalize<DK, DV>;
   e = hipFuncSetAttribute((const void*)kfin, hipFuncAttributeMaxDynamicSharedMemorySize, F.bytes);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kfin, dim3((unsigned)((n + C - 1) / C), (unsigned)BH), dim3(256), (size_t)F.bytes, s, q, k,

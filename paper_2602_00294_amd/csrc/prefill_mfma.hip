@@ -35,16 +35,23 @@
 // of one token, the update reads 4 tokens of 4 rows with the transposing
 // ds_read_b64_tr_b16.  Token rows are XOR-swizzled in 16-byte units.
 //
-// Work split.  The host packs pairs into slices (workgroups) that each own a
-// range of at most kMaxNC column groups, so every low feature is generated by
-// one slice only.  Each slice writes float32 partial readouts per token; a
-// second kernel adds them to the intra-chunk term and normalises.
+// Work split.  The host packs the pairs into slices (workgroups of 8 waves x
+// 8 pairs) that each cover a range of at most kMaxNC column groups; a slice
+// generates the low features of its range.  Inside a slice, runs of pairs
+// that share an epilogue (one kind and i1) are packed whole into waves, so
+// that no wave carries many runs.  Each slice writes float32 partial
+// readouts per token; a second kernel adds them to the intra-chunk term and
+// normalises.
 //
-// Per chunk, each workgroup runs two phases separated by a barrier:
-//   R: readout from phi(Q_c) and S_{c-1}      | generate phi(K_c), stage k~, v
-//   U: update of S with phi(K_c) and [V | k~] | generate phi(Q_{c+1}), flush O
-// Waves 0-3 run the matrix half first and waves 4-7 the vector half first, so
-// the two waves sharing a SIMD overlap matrix and vector work.
+// Per chunk, each workgroup runs two phases separated by barriers:
+//   U: update of S with phi(K_c) and [V | k~] | generate phi(Q_{c+1}), flush O_c
+//   R: readout from phi(Q_{c+1}) and S_c      | generate phi(K_{c+1}), stage k~, v
+// In U, waves 0-3 update first and waves 4-7 run the vector work first; R
+// has two halves, waves 0-3 reading out in the first and 4-7 in the second,
+// so the two waves that share a SIMD overlap matrix and vector work.  Each
+// run's readout is scaled into the SIMD's float32 sums in LDS.  Within the
+// matrix work, the next pair's operands are read while the current pair's
+// MFMAs run.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
