@@ -443,7 +443,7 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
         // pipeline over the slots: slot p+1's phi(K) operands are read while
         // slot p's MFMAs run, and a new run's B is built behind them.
         bf16x8 Bk[4];
-        auto build_b = [&](uint32_t m) __attribute__((always_inline)) {
+        auto build_b = [&](uint32_t m, bf16x8 (&Bk)[4]) __attribute__((always_inline)) {
           const uint32_t kind = s_kind(m);
 #pragma unroll
           for (int s = 0; s < 4; ++s) {
@@ -477,18 +477,30 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
             A[s] = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
           }
         };
-        bf16x8 Ac[4];
+        // B of the next run is built two slots ahead (into Bn), so its reads
+        // and arithmetic overlap two slots' MFMAs.
+        bf16x8 Ac[4], Bn[4];
         load_a(mt[0], Ac);
-        build_b(mt[0]);  // the first slot of a wave always starts a run
+        build_b(mt[0], Bk);  // the first slot of a wave always starts a run
+        if (PPW > 1 && (mt[PPW > 1 ? 1 : 0] & kFirst)) build_b(mt[PPW > 1 ? 1 : 0], Bn);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int p = 0; p < PPW; ++p) {
+          constexpr int kLastSlot = PPW - 1;
           bf16x8 An[4];
           if (p + 1 < PPW) load_a(mt[p + 1 < PPW ? p + 1 : p], An);
 #pragma unroll
           for (int s = 0; s < 4; ++s) S[p] = mfma32(Ac[s], Bk[s], S[p]);
           if (p + 1 < PPW) {
-            if (mt[p + 1 < PPW ? p + 1 : p] & kFirst) build_b(mt[p + 1 < PPW ? p + 1 : p]);
+            const uint32_t m1 = mt[p + 1 < PPW ? p + 1 : kLastSlot];
+            if (m1 & kFirst) {
+#pragma unroll
+              for (int s = 0; s < 4; ++s) Bk[s] = Bn[s];
+            }
+            if (p + 2 < PPW) {
+              const uint32_t m2 = mt[p + 2 < PPW ? p + 2 : kLastSlot];
+              if (m2 & kFirst) build_b(m2, Bn);
+            }
 #pragma unroll
             for (int s = 0; s < 4; ++s) Ac[s] = An[s];
           }
