@@ -131,16 +131,26 @@ __host__ __device__ constexpr LowFeat low_feat(int L) {
 
 __host__ __device__ constexpr int swap23(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
 
+// Value of low feature L from the unscaled coordinates x: the scale
+// d^(-p/4) of a degree-p feature is applied once, to its first factor, so
+// features that share a first index share that product.
+template <int DK>
+struct FeatScale {
+  static constexpr float deg1 = (float)(1.0 / 2.378414230005442);  // d^(-1/4) at d = 32
+  static constexpr float deg2 = (float)(1.0 / 5.656854249492381);  // d^(-1/2)
+  static constexpr float deg2sq = (float)(0.70710678118654752 / 5.656854249492381);  // with 1/sqrt(2!)
+};
 template <int DK, int L>
 __device__ __forceinline__ float low_value(const float (&x)[DK]) {
+  static_assert(DK == 32, "scale constants are for d = 32");
   constexpr LowFeat f = low_feat<DK>(L);
   if constexpr (f.deg == 2) {
     if constexpr (f.a == f.b)
-      return (x[f.a] * 0.70710678118654752f) * x[f.a];
+      return (x[f.a] * FeatScale<DK>::deg2sq) * x[f.a];
     else
-      return x[f.a] * x[f.b];
+      return (x[f.a] * FeatScale<DK>::deg2) * x[f.b];
   } else if constexpr (f.deg == 1) {
-    return x[f.a];
+    return x[f.a] * FeatScale<DK>::deg1;
   } else if constexpr (f.deg == 0) {
     return 1.0f;
   } else {
@@ -327,19 +337,19 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
       if (lid < 32 && pc < kC * DK / 8)
         *(uint4*)(smem + tile_off + (kC * (pc - tok * (DK / 8)) + tok) * 16) = w;
     };
-    // x~ = x d^(-1/4) of this lane's token from a raw tile
+    // the unscaled coordinates of this lane's token from a raw tile
     auto unpack_row = [&](int tile_off, float (&x)[DK]) __attribute__((always_inline)) {
 #pragma unroll
       for (int i = 0; i < DK / 8; ++i) {
         const uint4 w = *(const uint4*)(smem + tile_off + (kC * i + lane) * 16);
-        x[8 * i + 0] = bf_lo(w.x) * dscale;
-        x[8 * i + 1] = bf_hi(w.x) * dscale;
-        x[8 * i + 2] = bf_lo(w.y) * dscale;
-        x[8 * i + 3] = bf_hi(w.y) * dscale;
-        x[8 * i + 4] = bf_lo(w.z) * dscale;
-        x[8 * i + 5] = bf_hi(w.z) * dscale;
-        x[8 * i + 6] = bf_lo(w.w) * dscale;
-        x[8 * i + 7] = bf_hi(w.w) * dscale;
+        x[8 * i + 0] = bf_lo(w.x);
+        x[8 * i + 1] = bf_hi(w.x);
+        x[8 * i + 2] = bf_lo(w.y);
+        x[8 * i + 3] = bf_hi(w.y);
+        x[8 * i + 4] = bf_lo(w.z);
+        x[8 * i + 5] = bf_hi(w.z);
+        x[8 * i + 6] = bf_lo(w.w);
+        x[8 * i + 7] = bf_hi(w.w);
       }
     };
     // coordinates [4 wave, 4 wave + 4) of this lane's token from a raw tile
