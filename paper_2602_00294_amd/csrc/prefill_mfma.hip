@@ -596,6 +596,9 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
             }
           }
         };
+        // a zero operand the compiler cannot see through
+        bf16x8 zop = {};
+        asm volatile("" : "+v"(zop));
         uint4 bc[4];
         bf16x8 Ac[2];
         {
@@ -648,8 +651,9 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
                   *o = cur;
                 }
               }
-#pragma unroll
-              for (int j = 0; j < 16; ++j) R[t][j] = 0.0f;
+              // restart the sums on the matrix core (a zero product) instead
+              // of 16 vector moves
+              R[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(zop, zop, f32x16{}, 0, 0, 0);
             }
           }
           if (p + 1 < PPW) {
