@@ -198,6 +198,15 @@ __device__ __forceinline__ void gen_chain(const float (&x)[DK], int ulo, int uhi
     gen_chain<DK, U + kNW, NU>(x, ulo, uhi, row, sw16);
   }
 }
+// The same with the unit range [ULO, UHI) known at compile time, so that only
+// the coordinates the wave's units use are unpacked.
+template <int DK, int U, int NU, int ULO, int UHI>
+__device__ __forceinline__ void gen_chain_ct(const float (&x)[DK], char* row, int sw16) {
+  if constexpr (U < NU) {
+    if constexpr (U >= ULO && U < UHI) *(uint4*)(row + 64 * (U / 4) + ((16 * (U % 4)) ^ sw16)) = gen_unit<DK, U>(x);
+    gen_chain_ct<DK, U + kNW, NU, ULO, UHI>(x, row, sw16);
+  }
+}
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -359,22 +368,37 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
 
     // phi rows of the 64 tokens (lane = token); wave w writes the slice's units w, w + 8, ...
     const int sw16 = 16 * ((lane >> 2) & 3);
-    auto generate = [&](auto lower, const float (&x)[DK], char* dst) __attribute__((always_inline)) {
+    // Slices whose column groups start at 0 or end at the last group (the
+    // d = 32 plan has only these) generate with compile-time unit ranges; a
+    // slice starting at 0 may write groups past its own, inside its rows.
+    constexpr int kLoB = Low<DK>::NCG - kMaxNC;
+    const int gen_class = (lo == 0 && nc <= kMaxNC) ? 0 : (lo == kLoB && nc == kMaxNC) ? 1 : 2;
+    auto gen_wave = [&](auto W, int tile_off, char* row) __attribute__((always_inline)) {
+      constexpr int w = decltype(W)::value;
+      float x[DK];
+      unpack_row(tile_off, x);
+      if (gen_class == 0)
+        gen_chain_ct<DK, w, NU, 0, 4 * kMaxNC>(x, row, sw16);
+      else if (gen_class == 1)
+        gen_chain_ct<DK, w, NU, 4 * kLoB, 4 * (kLoB + kMaxNC)>(x, row, sw16);
+      else
+        gen_chain<DK, w, NU>(x, 4 * lo, 4 * (lo + nc), row, sw16);
+    };
+    auto generate = [&](auto lower, int tile_off, char* dst) __attribute__((always_inline)) {
       char* row = dst + lane * kPhiStride - 64 * lo;
-      const int ulo = 4 * lo, uhi = 4 * (lo + nc);
       if constexpr (decltype(lower)::value) {
         switch (wave) {
-          case 0: gen_chain<DK, 0, NU>(x, ulo, uhi, row, sw16); break;
-          case 1: gen_chain<DK, 1, NU>(x, ulo, uhi, row, sw16); break;
-          case 2: gen_chain<DK, 2, NU>(x, ulo, uhi, row, sw16); break;
-          default: gen_chain<DK, 3, NU>(x, ulo, uhi, row, sw16); break;
+          case 0: gen_wave(std::integral_constant<int, 0>{}, tile_off, row); break;
+          case 1: gen_wave(std::integral_constant<int, 1>{}, tile_off, row); break;
+          case 2: gen_wave(std::integral_constant<int, 2>{}, tile_off, row); break;
+          default: gen_wave(std::integral_constant<int, 3>{}, tile_off, row); break;
         }
       } else {
         switch (wave) {
-          case 4: gen_chain<DK, 4, NU>(x, ulo, uhi, row, sw16); break;
-          case 5: gen_chain<DK, 5, NU>(x, ulo, uhi, row, sw16); break;
-          case 6: gen_chain<DK, 6, NU>(x, ulo, uhi, row, sw16); break;
-          default: gen_chain<DK, 7, NU>(x, ulo, uhi, row, sw16); break;
+          case 4: gen_wave(std::integral_constant<int, 4>{}, tile_off, row); break;
+          case 5: gen_wave(std::integral_constant<int, 5>{}, tile_off, row); break;
+          case 6: gen_wave(std::integral_constant<int, 6>{}, tile_off, row); break;
+          default: gen_wave(std::integral_constant<int, 7>{}, tile_off, row); break;
         }
       }
     };
@@ -404,9 +428,7 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
         // raw k(c+1) in lanes [0, 32), raw v(c+1) in lanes [32, 64)
         const uint4 pkv = (lane < 32) ? load_piece(kh_, c + 1, lane) : load_piece(vh_, c + 1, lane - 32);
         if (c + 1 < nch) {
-          float x[DK];
-          unpack_row(L::RQ, x);
-          generate(lower, x, phiq);
+          generate(lower, L::RQ, phiq);
           const uint2 qd = quad(L::RQ);
           *(float4*)(xq + lane * kXS + 4 * wave) =
               float4{bf_lo(qd.x) * dscale, bf_hi(qd.x) * dscale, bf_lo(qd.y) * dscale, bf_hi(qd.y) * dscale};
@@ -527,9 +549,7 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
       const int cr = c + 1;
       auto vector_r = [&](auto lower) __attribute__((always_inline)) {
         const uint4 pq = load_piece(qh_, cr + 1, lane);  // raw q(c+2), lanes [0, 32)
-        float x[DK];
-        unpack_row(L::RK, x);
-        generate(lower, x, phik);
+        generate(lower, L::RK, phik);
         // k~ and v transposed: wave w takes dims [4 w, 4 w + 4) of every token
         const uint2 kd = quad(L::RK);
         const uint2 vd = quad(L::RV);
