@@ -265,8 +265,11 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
   const int tid = threadIdx.x;
   const int lane_id = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int slice = blockIdx.x;
-  const int64_t bh = blockIdx.y;
+  // Slice-major workgroup order: the hardware deals workgroups to the 8 XCDs
+  // in turn, so with heads innermost every XCD gets every slice kind (the
+  // kinds differ in cost) instead of a fixed one.
+  const int slice = (int)(blockIdx.x / (unsigned)BH);
+  const int64_t bh = blockIdx.x - (int64_t)slice * BH;
   const int4 sl = slices[slice];
   const int lo = __builtin_amdgcn_readfirstlane(sl.x);
   const int nc = __builtin_amdgcn_readfirstlane(sl.y);
@@ -1245,7 +1248,7 @@ hipError_t launch_typed(const u16* q, const u16* k, const u16* v, u16* y, float*
   auto kmain = prefill_mfma_main<DK, Ppw<DK>::value>;
   hipError_t e = hipFuncSetAttribute((const void*)kmain, hipFuncAttributeMaxDynamicSharedMemorySize, L::BYTES);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kmain, dim3((unsigned)dt.nslices, (unsigned)BH), dim3(kNW * 64), L::BYTES, s, q, k, v,
+  hipLaunchKernelGGL(kmain, dim3((unsigned)dt.nslices * (unsigned)BH), dim3(kNW * 64), L::BYTES, s, q, k, v,
                      dt.slices, dt.slots, dt.facs, dt.prep_idx, dt.prep_scale, dt.low_idx, partial, S_out, BH, n,
                      dt.nslices);
   if ((e = hipGetLastError()) != hipSuccess) return e;
