@@ -147,7 +147,7 @@ template <typename T, int NTH>
 __global__ void __launch_bounds__(NTH)
 decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __restrict__ k,
                    const T* __restrict__ v, T* __restrict__ y, const uint64_t* __restrict__ packed,
-                   const float* __restrict__ weight, int64_t D, int dk, int dv, int tu) {
+                   const float* __restrict__ weight, int64_t D, int dk, int dv, int tu, int P) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
   const int E = dv + 1;
   const int tid = threadIdx.x;
@@ -188,20 +188,58 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
   }
   for (int i = tid; i < E; i += NTH) ve[i] = (i < dv) ? to_f32(v[bh * dv + i]) : 1.0f;
   __syncthreads();
-  // the table entries of up to 8 features per thread are loaded together
-  for (int64_t fb = tid; fb < D; fb += 8 * NTH) {
-    uint64_t pk[8];
-    float w[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int64_t f = fb + (int64_t)NTH * u;
-      pk[u] = (f < D) ? packed[f] : 0;
-      w[u] = (f < D) ? weight[f] : 0.0f;
+  if (P == 4 && dk * (dk + 1) / 2 + dk + 1 <= NTH) {
+    // Features in closed form, no table: thread t < d(d+1)/2 takes the prefix
+    // (i1 <= i2) of rank t and writes the degree-2 feature (i1, i2) and the
+    // degree-3 features (i1, i2, i3), i3 = i2..d-1, at their canonical
+    // (degree-major, lexicographic) positions; the next d threads write
+    // degree 1 and one thread degree 0.  phi_m = prod x~[m_j] / sqrt(prod c!),
+    // x~ = x d^(-1/4).
+    const float s4 = 1.0f / sqrtf(sqrtf((float)dk));
+    const int npair = dk * (dk + 1) / 2;
+    const int64_t base2 = 1 + dk, base3 = 1 + dk + npair;
+    if (tid < npair) {
+      int i1 = 0, r = tid;
+      while (r >= dk - i1) {
+        r -= dk - i1;
+        ++i1;
+      }
+      const int i2 = i1 + r;
+      const float qa = xq[i1] * s4, qb = xq[i2] * s4, ka = xk[i1] * s4, kb = xk[i2] * s4;
+      const float w2 = (i1 == i2) ? 0.70710678118654752f : 1.0f;
+      fkq[base2 + tid] = float2{ka * kb * w2, qa * qb * w2};
+      // degree-3 tuples before (i1, i2, .): all with a smaller first index, then
+      // first index i1 and second index in [i1, i2)
+      const int64_t c3 = (int64_t)(dk + 2) * (dk + 1) * dk / 6 - (int64_t)(dk - i1 + 2) * (dk - i1 + 1) * (dk - i1) / 6;
+      const int64_t f3 = base3 + c3 + (int64_t)(i2 - i1) * dk - ((int64_t)i2 * (i2 - 1) - (int64_t)i1 * (i1 - 1)) / 2;
+      const float pq = qa * qb, pk = ka * kb;
+      for (int i3 = i2; i3 < dk; ++i3) {
+        // 1 / sqrt(prod c!): 1/sqrt(6) for three equal indices, 1/sqrt(2) for two
+        const float w3 = (i1 == i3) ? 0.40824829046386302f : ((i1 == i2 || i2 == i3) ? 0.70710678118654752f : 1.0f);
+        fkq[f3 + (i3 - i2)] = float2{pk * (xk[i3] * s4) * w3, pq * (xq[i3] * s4) * w3};
+      }
+    } else if (tid < npair + dk) {
+      const int i = tid - npair;
+      fkq[1 + i] = float2{xk[i] * s4, xq[i] * s4};
+    } else if (tid == npair + dk) {
+      fkq[0] = float2{1.0f, 1.0f};
     }
+  } else {
+    // the table entries of up to 8 features per thread are loaded together
+    for (int64_t fb = tid; fb < D; fb += 8 * NTH) {
+      uint64_t pk[8];
+      float w[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int64_t f = fb + (int64_t)NTH * u;
-      if (f < D) fkq[f] = float2{feature_value(pk[u], w[u], xk), feature_value(pk[u], w[u], xq)};
+      for (int u = 0; u < 8; ++u) {
+        const int64_t f = fb + (int64_t)NTH * u;
+        pk[u] = (f < D) ? packed[f] : 0;
+        w[u] = (f < D) ? weight[f] : 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int64_t f = fb + (int64_t)NTH * u;
+        if (f < D) fkq[f] = float2{feature_value(pk[u], w[u], xk), feature_value(pk[u], w[u], xq)};
+      }
     }
   }
   __syncthreads();
@@ -538,7 +576,7 @@ hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, 
   if (e != hipSuccess) return e;                                                                          \
   hipLaunchKernelGGL((decode_flat_kernel<TT, 1024>), dim3((unsigned)BH), dim3(1024), plan.flat_lds, s, S,  \
                      (const TT*)q, (const TT*)k, (const TT*)v, (TT*)y, t.packed, t.weight, t.D, dk, dv,   \
-                     plan.flat_tu)
+                     plan.flat_tu, t.P)
     if (bf16) { SATA_DECODE_FLAT(bf16_t); } else { SATA_DECODE_FLAT(float); }
 #undef SATA_DECODE_FLAT
     return hipGetLastError();
