@@ -326,6 +326,14 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
       mt[p] = meta[p];
       asm volatile("" : "+s"(mt[p]));
     }
+    // Each use takes the descriptor through another empty asm, so values
+    // derived from it are formed where they are used rather than kept in
+    // scalar registers across the iteration.
+    auto M = [&](int p) __attribute__((always_inline)) -> uint32_t {
+      uint32_t m = mt[p];
+      asm volatile("" : "+s"(m));
+      return m;
+    };
     // The lane index likewise, so per-lane addresses are recomputed each
     // iteration instead of being kept (and spilled) across the loop.
     int lane = lane_id;
@@ -515,25 +523,25 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
         // B of the next run is built two slots ahead (into Bn), so its reads
         // and arithmetic overlap two slots' MFMAs.
         bf16x8 Ac[4], Bn[4];
-        load_a(mt[0], Ac);
-        build_b(mt[0], Bk);  // the first slot of a wave always starts a run
-        if (PPW > 1 && (mt[PPW > 1 ? 1 : 0] & kFirst)) build_b(mt[PPW > 1 ? 1 : 0], Bn);
+        load_a(M(0), Ac);
+        build_b(M(0), Bk);  // the first slot of a wave always starts a run
+        if (PPW > 1 && (M(PPW > 1 ? 1 : 0) & kFirst)) build_b(M(PPW > 1 ? 1 : 0), Bn);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int p = 0; p < PPW; ++p) {
           constexpr int kLastSlot = PPW - 1;
           bf16x8 An[4];
-          if (p + 1 < PPW) load_a(mt[p + 1 < PPW ? p + 1 : p], An);
+          if (p + 1 < PPW) load_a(M(p + 1 < PPW ? p + 1 : p), An);
 #pragma unroll
           for (int s = 0; s < 4; ++s) S[p] = mfma32(Ac[s], Bk[s], S[p]);
           if (p + 1 < PPW) {
-            const uint32_t m1 = mt[p + 1 < PPW ? p + 1 : kLastSlot];
+            const uint32_t m1 = M(p + 1 < PPW ? p + 1 : kLastSlot);
             if (m1 & kFirst) {
 #pragma unroll
               for (int s = 0; s < 4; ++s) Bk[s] = Bn[s];
             }
             if (p + 2 < PPW) {
-              const uint32_t m2 = mt[p + 2 < PPW ? p + 2 : kLastSlot];
+              const uint32_t m2 = M(p + 2 < PPW ? p + 2 : kLastSlot);
               if (m2 & kFirst) build_b(m2, Bn);
             }
 #pragma unroll
@@ -626,14 +634,14 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
         bf16x8 Ac[2];
         {
           float4 fw[4];
-          load_b(mt[0], bc);
-          load_fac(mt[0], fw);
-          convert(S[0], mt[0], fw, Ac);
+          load_b(M(0), bc);
+          load_fac(M(0), fw);
+          convert(S[0], M(0), fw, Ac);
         }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int p = 0; p < PPW; ++p) {
-          const uint32_t m = mt[p];
+          const uint32_t m = M(p);
           R[0] = mfma32(Ac[0], __builtin_bit_cast(bf16x8, bc[0]), R[0]);
           R[0] = mfma32(Ac[1], __builtin_bit_cast(bf16x8, bc[1]), R[0]);
           R[1] = mfma32(Ac[0], __builtin_bit_cast(bf16x8, bc[2]), R[1]);
@@ -642,8 +650,8 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
           float4 fw[4];
           bf16x8 An[2];
           if (p + 1 < PPW) {
-            load_b(mt[p + 1], bn);
-            load_fac(mt[p + 1], fw);
+            load_b(M(p + 1), bn);
+            load_fac(M(p + 1), fw);
           }
           if (m & kLast) {
             // run epilogue into this SIMD's sums: scale by q~[:, i1] (TOP), 1
@@ -680,7 +688,7 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
             }
           }
           if (p + 1 < PPW) {
-            convert(S[p + 1 < PPW ? p + 1 : p], mt[p + 1 < PPW ? p + 1 : p], fw, An);
+            convert(S[p + 1 < PPW ? p + 1 : p], M(p + 1 < PPW ? p + 1 : p), fw, An);
 #pragma unroll
             for (int i = 0; i < 4; ++i) bc[i] = bn[i];
             Ac[0] = An[0];
