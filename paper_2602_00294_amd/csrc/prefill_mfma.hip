@@ -752,9 +752,9 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
 
 struct FinLayout {
   int qs, ps, vs;             // row strides in bytes
-  int oq, ok, op, ov, oz, orow, opart;  // byte offsets
+  int oq, ok, op, ov, oz, orow;  // byte offsets
   int bytes;
-  __host__ __device__ FinLayout(int DK, int DV, int C, int PS) {
+  __host__ __device__ FinLayout(int DK, int DV, int C) {
     qs = DK * 2 + 16;
     ps = C * 2 + 16;
     vs = C * 2 + 16;
@@ -764,8 +764,7 @@ struct FinLayout {
     ov = op + C * ps;
     oz = ov + DV * vs;
     orow = oz + C * 4;
-    opart = orow + C * (C / 16) * 4;  // float [C][PS]: the slices' partials, summed
-    bytes = opart + C * PS * 4;
+    bytes = orow + C * (C / 16) * 4;
   }
 };
 
@@ -780,7 +779,7 @@ prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, cons
                       int P, int PS) {
   constexpr int E = DV + 1;
   constexpr int NT = DV / 16;
-  const FinLayout L(DK, DV, C, PS);
+  const FinLayout L(DK, DV, C);
   extern __shared__ __attribute__((aligned(16))) char smem[];
   char* Qs = smem + L.oq;
   char* Ks = smem + L.ok;
@@ -788,7 +787,6 @@ prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, cons
   char* Vt = smem + L.ov;
   float* Zs = (float*)(smem + L.oz);
   float* rowpart = (float*)(smem + L.orow);  // [query][key tile]
-  float* psum = (float*)(smem + L.opart);    // [query][PS]
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int l15 = lane & 15;
@@ -822,29 +820,6 @@ prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, cons
     for (int e = 0; e < 4; ++e) {
       *(u16*)(Vt + (c8 + 2 * e) * L.vs + tok * 2) = (u16)w[e];
       *(u16*)(Vt + (c8 + 2 * e + 1) * L.vs + tok * 2) = (u16)(w[e] >> 16);
-    }
-  }
-  // the slices' partials of the chunk, added in slice order: 8 float4 value
-  // pieces and the normaliser per token
-  for (int i = tid; i < C * (DV / 4 + 1); i += 256) {
-    const int tok = i / (DV / 4 + 1);
-    const int pc = i - tok * (DV / 4 + 1);
-    if (pc < DV / 4) {
-      float4 a = {0.0f, 0.0f, 0.0f, 0.0f};
-      if (tok < cn)
-        for (int s = 0; s < nslices; ++s) {
-          const float4 w = *(const float4*)(partial + (((int64_t)s * BH + bh) * n + t0 + tok) * PS + 4 * pc);
-          a.x += w.x;
-          a.y += w.y;
-          a.z += w.z;
-          a.w += w.w;
-        }
-      *(float4*)(psum + tok * PS + 4 * pc) = a;
-    } else {
-      float a = 0.0f;
-      if (tok < cn)
-        for (int s = 0; s < nslices; ++s) a += partial[(((int64_t)s * BH + bh) * n + t0 + tok) * PS + DV];
-      psum[tok * PS + DV] = a;
     }
   }
   __syncthreads();
@@ -887,7 +862,8 @@ prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, cons
   for (int qi = tid; qi < C; qi += 256) {
     float z = (float)t0;
     for (int t = 0; t < MT; ++t) z += rowpart[qi * MT + t];
-    z += psum[qi * PS + DV];
+    if (qi < cn)
+      for (int s = 0; s < nslices; ++s) z += partial[(((int64_t)s * BH + bh) * n + t0 + qi) * PS + DV];
     Zs[qi] = z;
   }
   __syncthreads();
@@ -908,7 +884,8 @@ prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, cons
       const int qi = 16 * mq + 4 * g4 + i;
       const int col = 16 * j + l15;
       if (qi < cn) {
-        const float o = acc[i] + psum[qi * PS + col];
+        float o = acc[i];
+        for (int s = 0; s < nslices; ++s) o += partial[(((int64_t)s * BH + bh) * n + t0 + qi) * PS + col];
         y[(bh * n + t0 + qi) * DV + col] = f32_to_bf16(o / Zs[qi]).bits;
       }
     }
@@ -1260,7 +1237,7 @@ hipError_t launch_typed(const u16* q, const u16* k, const u16* v, u16* y, float*
                      dt.slices, dt.slots, dt.facs, dt.prep_idx, dt.prep_scale, dt.low_idx, partial, S_out, BH, n,
                      dt.nslices);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  const FinLayout F(DK, DK, kC, kPS);
+  const FinLayout F(DK, DK, kC);
   auto kfin = prefill_mfma_finalize<DK, DK>;
   e = hipFuncSetAttribute((const void*)kfin, hipFuncAttributeMaxDynamicSharedMemorySize, F.bytes);
   if (e != hipSuccess) return e;
