@@ -77,6 +77,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned short u16;
 
 constexpr int kC = 64;        // tokens per chunk
+static_assert(kC == 64, "the finalize splits a chunk into 16 score tiles over 4 waves");
 constexpr int kNW = 8;        // waves per workgroup
 constexpr int kMaxNC = 9;     // column groups per slice
 constexpr int kTS = 68;       // floats per row of the transposed float32 tiles
@@ -760,8 +761,8 @@ struct FinLayout {
     vs = C * 2 + 16;
     oq = 0;
     ok = oq + C * qs;
-    op = ok + C * qs;
-    ov = op + C * ps;
+    op = 0;  // the weights overwrite Q and K once the scores are in registers
+    ov = (C * ps > 2 * C * qs) ? C * ps : 2 * C * qs;
     oz = ov + DV * vs;
     orow = oz + C * 4;
     bytes = orow + C * (C / 16) * 4;
@@ -824,12 +825,17 @@ prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, cons
   }
   __syncthreads();
 
-  // scores and Taylor weights, one 16x16 tile per step; row sums per tile
-  for (int tile = wave; tile < MT * MT; tile += 4) {
+  // scores, one 16x16 tile per step, kept in registers; then the Taylor
+  // weights (bf16, over the Q and K tiles) and their row sums per tile
+  constexpr int kTilesPerWave = 4;  // (64 / 16)^2 tiles over 4 waves
+  f32x4 sc[kTilesPerWave];
+#pragma unroll
+  for (int it = 0; it < kTilesPerWave; ++it) {
+    const int tile = wave + 4 * it;
     const int mq = tile / MT;
     const int nk = tile - mq * MT;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    if (nk <= mq) {
+    if (tile < MT * MT && nk <= mq) {
 #pragma unroll
       for (int kk = 0; kk < (DK + 31) / 32; ++kk) {
         uint4 aw = {0u, 0u, 0u, 0u}, bw = {0u, 0u, 0u, 0u};
@@ -840,6 +846,16 @@ prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, cons
         acc = mfma16(__builtin_bit_cast(bf16x8, aw), __builtin_bit_cast(bf16x8, bw), acc);
       }
     }
+    sc[it] = acc;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int it = 0; it < kTilesPerWave; ++it) {
+    const int tile = wave + 4 * it;
+    if (tile >= MT * MT) break;
+    const int mq = tile / MT;
+    const int nk = tile - mq * MT;
+    const f32x4 acc = sc[it];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int qi = 16 * mq + 4 * g4 + i;
