@@ -774,7 +774,7 @@ __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
 }
 
 template <int DK, int DV>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(256, 8)
 prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, const u16* __restrict__ v,
                       const float* __restrict__ partial, u16* __restrict__ y, int BH, int n, int C, int nslices,
                       int P, int PS) {
@@ -798,6 +798,31 @@ prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, cons
   const int cn = min(C, n - t0);
   const float inv_sqrt_d = 1.0f / sqrtf((float)DK);
   const int MT = C / 16;
+
+  // The slices' partials this thread adds in the epilogues are loaded first,
+  // so that their latency overlaps the staging and the scores: the output
+  // entries of its two (query, value) tiles, and (threads < C) one normaliser.
+  constexpr int kOutTilesPerWave = 2;  // (64 / 16) x (32 / 16) tiles over 4 waves
+  static_assert(DV == 32, "two value tiles");
+  float pre[kOutTilesPerWave][4];
+#pragma unroll
+  for (int it = 0; it < kOutTilesPerWave; ++it) {
+    const int tile = wave + 4 * it;
+    const int mq = tile / NT;
+    const int j = tile - mq * NT;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int qi = 16 * mq + 4 * g4 + i;
+      const int col = 16 * j + l15;
+      float a = 0.0f;
+      if (qi < cn)
+        for (int s = 0; s < nslices; ++s) a += partial[(((int64_t)s * BH + bh) * n + t0 + qi) * PS + col];
+      pre[it][i] = a;
+    }
+  }
+  float prez = 0.0f;
+  if (tid < cn)
+    for (int s = 0; s < nslices; ++s) prez += partial[(((int64_t)s * BH + bh) * n + t0 + tid) * PS + DV];
 
   // stage Q, K rows and V^T (bf16), 8 coordinates per thread; tokens >= cn are zero
   for (int i = tid; i < C * (DK / 8); i += 256) {
@@ -875,17 +900,17 @@ prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, cons
   __syncthreads();
 
   // normaliser: intra row sums + partials + earlier-token count (degree 0)
-  for (int qi = tid; qi < C; qi += 256) {
+  if (tid < C) {
     float z = (float)t0;
-    for (int t = 0; t < MT; ++t) z += rowpart[qi * MT + t];
-    if (qi < cn)
-      for (int s = 0; s < nslices; ++s) z += partial[(((int64_t)s * BH + bh) * n + t0 + qi) * PS + DV];
-    Zs[qi] = z;
+    for (int t = 0; t < MT; ++t) z += rowpart[tid * MT + t];
+    Zs[tid] = z + prez;
   }
   __syncthreads();
 
   // O = P V on the matrix cores, + partials, / Z
-  for (int tile = wave; tile < MT * NT; tile += 4) {
+#pragma unroll
+  for (int it = 0; it < kOutTilesPerWave; ++it) {
+    const int tile = wave + 4 * it;
     const int mq = tile / NT;
     const int j = tile - mq * NT;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -899,11 +924,7 @@ prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, cons
     for (int i = 0; i < 4; ++i) {
       const int qi = 16 * mq + 4 * g4 + i;
       const int col = 16 * j + l15;
-      if (qi < cn) {
-        float o = acc[i];
-        for (int s = 0; s < nslices; ++s) o += partial[(((int64_t)s * BH + bh) * n + t0 + qi) * PS + col];
-        y[(bh * n + t0 + qi) * DV + col] = f32_to_bf16(o / Zs[qi]).bits;
-      }
+      if (qi < cn) y[(bh * n + t0 + qi) * DV + col] = f32_to_bf16((acc[i] + pre[it][i]) / Zs[qi]).bits;
     }
   }
 }
