@@ -800,25 +800,29 @@ prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, cons
   const int MT = C / 16;
 
   // The slices' partials this thread adds in the epilogues are loaded first,
-  // so that their latency overlaps the staging and the scores: the output
-  // entries of its two (query, value) tiles, and (threads < C) one normaliser.
+  // so that their latency overlaps the staging and the scores: for each of
+  // its two output tiles (computed transposed, so a lane holds 4 consecutive
+  // value columns of one query) one float4 per slice, and (threads < C) one
+  // normaliser.
   constexpr int kOutTilesPerWave = 2;  // (64 / 16) x (32 / 16) tiles over 4 waves
   static_assert(DV == 32, "two value tiles");
-  float pre[kOutTilesPerWave][4];
+  float4 pre[kOutTilesPerWave];
 #pragma unroll
   for (int it = 0; it < kOutTilesPerWave; ++it) {
     const int tile = wave + 4 * it;
     const int mq = tile / NT;
     const int j = tile - mq * NT;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int qi = 16 * mq + 4 * g4 + i;
-      const int col = 16 * j + l15;
-      float a = 0.0f;
-      if (qi < cn)
-        for (int s = 0; s < nslices; ++s) a += partial[(((int64_t)s * BH + bh) * n + t0 + qi) * PS + col];
-      pre[it][i] = a;
-    }
+    const int qi = 16 * mq + l15;
+    float4 a = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (qi < cn)
+      for (int s = 0; s < nslices; ++s) {
+        const float4 w = *(const float4*)(partial + (((int64_t)s * BH + bh) * n + t0 + qi) * PS + 16 * j + 4 * g4);
+        a.x += w.x;
+        a.y += w.y;
+        a.z += w.z;
+        a.w += w.w;
+      }
+    pre[it] = a;
   }
   float prez = 0.0f;
   if (tid < cn)
@@ -907,7 +911,8 @@ prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, cons
   }
   __syncthreads();
 
-  // O = P V on the matrix cores, + partials, / Z
+  // O^T = V^T P^T on the matrix cores, + partials, / Z: lane (l15, g4) ends up
+  // with value columns 16 j + 4 g4 + 0..3 of query 16 mq + l15
 #pragma unroll
   for (int it = 0; it < kOutTilesPerWave; ++it) {
     const int tile = wave + 4 * it;
@@ -916,15 +921,17 @@ prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, cons
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int ks = 0; ks * 32 < C; ++ks) {
       if (32 * ks > 16 * mq + 15) break;  // keys beyond the tile's last query carry zero weight
-      const uint4 aw = *(const uint4*)(Pm + (16 * mq + l15) * L.ps + (32 * ks + 8 * g4) * 2);
-      const uint4 bw = *(const uint4*)(Vt + (16 * j + l15) * L.vs + (32 * ks + 8 * g4) * 2);
-      acc = mfma16(__builtin_bit_cast(bf16x8, aw), __builtin_bit_cast(bf16x8, bw), acc);
+      const uint4 pw = *(const uint4*)(Pm + (16 * mq + l15) * L.ps + (32 * ks + 8 * g4) * 2);
+      const uint4 vw = *(const uint4*)(Vt + (16 * j + l15) * L.vs + (32 * ks + 8 * g4) * 2);
+      acc = mfma16(__builtin_bit_cast(bf16x8, vw), __builtin_bit_cast(bf16x8, pw), acc);
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int qi = 16 * mq + 4 * g4 + i;
-      const int col = 16 * j + l15;
-      if (qi < cn) y[(bh * n + t0 + qi) * DV + col] = f32_to_bf16((acc[i] + pre[it][i]) / Zs[qi]).bits;
+    const int qi = 16 * mq + l15;
+    if (qi < cn) {
+      const float z = Zs[qi];
+      uint2 w;
+      w.x = (uint32_t)f32_to_bf16((acc[0] + pre[it].x) / z).bits | ((uint32_t)f32_to_bf16((acc[1] + pre[it].y) / z).bits << 16);
+      w.y = (uint32_t)f32_to_bf16((acc[2] + pre[it].z) / z).bits | ((uint32_t)f32_to_bf16((acc[3] + pre[it].w) / z).bits << 16);
+      *(uint2*)(y + (bh * n + t0 + qi) * DV + 16 * j + 4 * g4) = w;
     }
   }
 }
