@@ -439,14 +439,6 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
       auto vector_u = [&](auto lower) __attribute__((always_inline)) {
         // raw k(c+1) in lanes [0, 32), raw v(c+1) in lanes [32, 64)
         const uint4 pkv = (lane < 32) ? load_piece(kh_, c + 1, lane) : load_piece(vh_, c + 1, lane - 32);
-        if (c + 1 < nch) {
-          generate(lower, L::RQ, phiq);
-          const uint2 qd = quad(L::RQ);
-          *(float4*)(xq + lane * kXS + 4 * wave) =
-              float4{bf_lo(qd.x) * dscale, bf_hi(qd.x) * dscale, bf_lo(qd.y) * dscale, bf_hi(qd.y) * dscale};
-        }
-        // (kept apart from the generation so that their registers do not overlap)
-        __builtin_amdgcn_sched_barrier(0);
         if (c >= 0) {
           // the four per-SIMD readout sums of chunk c -> this slice's partial
           // (rows of kPS floats: 32 values, the normaliser), clearing them; 8
@@ -475,6 +467,15 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
             *(float4*)(dst + cq) = o;
             if (cq == 0) dst[DV] = z;
           }
+        }
+        // (the flush first: its LDS reads then do not queue behind the feature
+        // writes; kept apart so that their registers do not overlap)
+        __builtin_amdgcn_sched_barrier(0);
+        if (c + 1 < nch) {
+          generate(lower, L::RQ, phiq);
+          const uint2 qd = quad(L::RQ);
+          *(float4*)(xq + lane * kXS + 4 * wave) =
+              float4{bf_lo(qd.x) * dscale, bf_hi(qd.x) * dscale, bf_lo(qd.y) * dscale, bf_hi(qd.y) * dscale};
         }
         if (lane < 32)
           store_piece(L::RK, lane, pkv);
