@@ -651,10 +651,6 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
           uint4 bn[4];
           float4 fw[4];
           bf16x8 An[2];
-          if (p + 1 < PPW) {
-            load_b(M(p + 1), bn);
-            load_fac(M(p + 1), fw);
-          }
           if (m & kLast) {
             // run epilogue into this SIMD's sums: scale by q~[:, i1] (TOP), 1
             // (LOW) or contract with q~ (ZMAT).  Each lane owns its entries.
@@ -688,6 +684,12 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
               // of 16 vector moves
               R[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(zop, zop, f32x16{}, 0, 0, 0);
             }
+          }
+          // the next slot's operands are read after the epilogue's LDS accesses,
+          // which would otherwise queue behind them
+          if (p + 1 < PPW) {
+            load_b(M(p + 1), bn);
+            load_fac(M(p + 1), fw);
           }
           if (p + 1 < PPW) {
             convert(S[p + 1 < PPW ? p + 1 : p], M(p + 1 < PPW ? p + 1 : p), fw, An);
