@@ -524,17 +524,16 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
         };
         // B of the next run is built two slots ahead (into Bn), so its reads
         // and arithmetic overlap two slots' MFMAs.
-        bf16x8 Ac[4], An[4], Bn[4];
+        bf16x8 Ac[4], Bn[4];
         load_a(M(0), Ac);
-        if (PPW > 1) load_a(M(PPW > 1 ? 1 : 0), An);  // phi(K) operands run two slots ahead
         build_b(M(0), Bk);  // the first slot of a wave always starts a run
         if (PPW > 1 && (M(PPW > 1 ? 1 : 0) & kFirst)) build_b(M(PPW > 1 ? 1 : 0), Bn);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int p = 0; p < PPW; ++p) {
           constexpr int kLastSlot = PPW - 1;
-          bf16x8 A2[4];
-          if (p + 2 < PPW) load_a(M(p + 2 < PPW ? p + 2 : p), A2);
+          bf16x8 An[4];
+          if (p + 1 < PPW) load_a(M(p + 1 < PPW ? p + 1 : p), An);
 #pragma unroll
           for (int s = 0; s < 4; ++s) S[p] = mfma32(Ac[s], Bk[s], S[p]);
           if (p + 1 < PPW) {
@@ -548,10 +547,7 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
               if (m2 & kFirst) build_b(m2, Bn);
             }
 #pragma unroll
-            for (int s = 0; s < 4; ++s) {
-              Ac[s] = An[s];
-              An[s] = A2[s];
-            }
+            for (int s = 0; s < 4; ++s) Ac[s] = An[s];
           }
           __builtin_amdgcn_sched_barrier(0);
         }
@@ -655,6 +651,10 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
           uint4 bn[4];
           float4 fw[4];
           bf16x8 An[2];
+          if (p + 1 < PPW) {
+            load_b(M(p + 1), bn);
+            load_fac(M(p + 1), fw);
+          }
           if (m & kLast) {
             // run epilogue into this SIMD's sums: scale by q~[:, i1] (TOP), 1
             // (LOW) or contract with q~ (ZMAT).  Each lane owns its entries.
@@ -688,12 +688,6 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
               // of 16 vector moves
               R[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(zop, zop, f32x16{}, 0, 0, 0);
             }
-          }
-          // the next slot's operands are read after the epilogue's LDS accesses,
-          // which would otherwise queue behind them
-          if (p + 1 < PPW) {
-            load_b(M(p + 1), bn);
-            load_fac(M(p + 1), fw);
           }
           if (p + 1 < PPW) {
             convert(S[p + 1 < PPW ? p + 1 : p], M(p + 1 < PPW ? p + 1 : p), fw, An);
