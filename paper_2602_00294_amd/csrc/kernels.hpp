@@ -26,11 +26,15 @@ struct DecodePlan {
   int threads = 0;  // workgroup size
   int flat_tu = 0;  // > 0: whole-head float4 streaming kernel with this many threads in use
   size_t flat_lds = 0;
+  int flat_msplit = 0;  // > 0: two workgroups per head, split after this many steps per thread
 };
 DecodePlan plan_decode(int64_t D, int dk, int dv);
+// partial: BH * nslices * (dv + 1) floats when nslices > 1, BH * 2 * (dv + 1)
+// when flat_msplit > 0; counters: BH ints, all zero, when flat_msplit > 0 (the
+// kernel leaves them zero).  Without them a split plan runs unsplit.
 hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, void* y, bool bf16,
                          int BH, int dk, int dv, const DevTable& t, const DecodePlan& plan,
-                         float* partial, hipStream_t s);
+                         float* partial, int* counters, hipStream_t s);
 
 // ---- prefill, generic float32 path --------------------------------------------
 struct PrefillGenericPlan {

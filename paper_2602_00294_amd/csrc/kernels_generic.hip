@@ -129,6 +129,10 @@ decode_head_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
   for (int j = threadIdx.x; j < dv; j += NTH) y[bh * dv + j] = from_f32<T>(red[j] / red[dv]);
 }
 
+// Workgroup barrier over LDS data only.  __syncthreads also waits for the
+// thread's outstanding global loads; this one lets them stay in flight.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // Whole-head decode as one flat float4 stream.  A head's state is D*E
 // contiguous floats (E = d_v + 1).  Of the workgroup's threads, tu (a multiple
 // of E / gcd(E, 4)) take part: thread t owns the float4s g = t + tu*m of the
@@ -141,17 +145,36 @@ decode_head_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
 // start by threads of their own and their readout terms added in element
 // order at the end, so the result is deterministic.  Loads run two groups of
 // kFlatUnroll float4s ahead of the arithmetic.
+//
+// With xpart given, each head is streamed by two workgroups (blockIdx =
+// 2 head + piece): piece 0 takes a thread's steps m < msplit, piece 1 the
+// rest.  The hardware deals workgroups to the 8 XCDs in turn, so piece 0 runs
+// on the even-numbered XCDs and piece 1 on the odd ones, which stream this
+// pattern about a quarter more slowly; msplit sizes the pieces to match.
+// Each piece stores its E column sums at xpart[2 head + piece] with device-
+// coherent stores and bumps cnt[head]; the second to arrive adds the two (a
+// sum of two terms, so the result does not depend on which one it is), writes
+// y and sets the counter back to 0.  No device-scope fence is used: one would
+// write back the XCD's whole L2, full of freshly written state.
 constexpr int kFlatUnroll = 2;
+// Share of a head's stream given to the piece on an even-numbered XCD: their
+// measured streaming times for this pattern are 47 and 59 us per head.
+constexpr double kFlatEvenShare = 0.557;
 
 template <typename T, int NTH>
-__global__ void __launch_bounds__(NTH)
+__global__ void __launch_bounds__(NTH, 8)
 decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __restrict__ k,
                    const T* __restrict__ v, T* __restrict__ y, const uint64_t* __restrict__ packed,
-                   const float* __restrict__ weight, int64_t D, int dk, int dv, int tu, int P) {
+                   const float* __restrict__ weight, int64_t D, int dk, int dv, int tu, int P,
+                   int msplit, float* __restrict__ xpart, int* __restrict__ cnt) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
   const int E = dv + 1;
   const int tid = threadIdx.x;
-  const int64_t bh = blockIdx.x;
+  const bool split = xpart != nullptr;
+  const int piece = split ? (int)(blockIdx.x & 1) : 0;
+  const int64_t bh = split ? (int64_t)(blockIdx.x >> 1) : (int64_t)blockIdx.x;
+  const int64_t m_lo = piece ? msplit : 0;
+  const int64_t m_hi = (split && piece == 0) ? msplit : ((int64_t)1 << 40);
   const int64_t N = D * E;
   float* const Sh = S + bh * N;
   float2* const fkq = (float2*)lds;        // [D] {phi_k, phi_q}
@@ -170,60 +193,78 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
   const bool active = tid < tu;
   // leftover elements [0, a0) and [a0 + 4 nv, N): one per thread of the last wave
   const int nlead = (int)min<int64_t>(a0, N);
-  const int nleft = nlead + (int)(N - (a0 + 4 * nv));
+  const int nleft = piece ? 0 : nlead + (int)(N - (a0 + 4 * nv));
   const int lt = tid - (NTH - 8);
   const int64_t le = (lt < nlead) ? lt : a0 + 4 * nv + (lt - nlead);
-  float lx = 0.0f;
-  if (lt >= 0 && lt < nleft) lx = Sh[le];
-  // the first loads go out before the features are computed
+  // q, k, v go to LDS first (in the first wave, which waits for them there),
+  // then every wave sends its first state loads, which stay in flight while
+  // the features are computed: the barriers below wait for LDS only
+  if (tid < dk) {
+    xq[tid] = to_f32(q[bh * dk + tid]);
+    xk[tid] = to_f32(k[bh * dk + tid]);
+  }
+  if (tid < E) ve[tid] = (tid < dv) ? to_f32(v[bh * dv + tid]) : 1.0f;
+  // (branch-free: an out-of-range slot reads element 0, which the stream skips)
+  const bool lead = lt >= 0 && lt < nleft;
+  float lx = Sh[lead ? le : 0];
   float4 cur[kFlatUnroll];
 #pragma unroll
   for (int u = 0; u < kFlatUnroll; ++u) {
-    const int64_t g = tid + (int64_t)tu * u;
-    cur[u] = (active && g < nv) ? Sv[g] : float4{0.0f, 0.0f, 0.0f, 0.0f};
+    const int64_t g = tid + (int64_t)tu * (m_lo + u);
+    cur[u] = Sv[(active && g < nv && m_lo + u < m_hi) ? g : 0];
   }
-  for (int i = tid; i < dk; i += NTH) {
-    xq[i] = to_f32(q[bh * dk + i]);
-    xk[i] = to_f32(k[bh * dk + i]);
-  }
-  for (int i = tid; i < E; i += NTH) ve[i] = (i < dv) ? to_f32(v[bh * dv + i]) : 1.0f;
-  __syncthreads();
-  if (P == 4 && dk * (dk + 1) / 2 + dk + 1 <= NTH) {
-    // Features in closed form, no table: thread t < d(d+1)/2 takes the prefix
-    // (i1 <= i2) of rank t and writes the degree-2 feature (i1, i2) and the
-    // degree-3 features (i1, i2, i3), i3 = i2..d-1, at their canonical
-    // (degree-major, lexicographic) positions; the next d threads write
-    // degree 1 and one thread degree 0.  phi_m = prod x~[m_j] / sqrt(prod c!),
-    // x~ = x d^(-1/4).
+  lx = lead ? lx : 0.0f;
+  lds_barrier();
+  if (P == 4) {
+    // Features in closed form, no table.  Work items are (prefix i1 <= i2,
+    // block h of up to 8 third indices i3 in [i2 + 8h, i2 + 8h + 8)); tier h
+    // holds the prefixes with i2 < d - 8h, numbered i2-major (rank
+    // i2 (i2 + 1) / 2 + i1), so a thread's item decodes without a search
+    // and none walks more than 8 features.  Tier 0 also writes the degree-2
+    // feature (i1, i2); the last threads write degrees 0 and 1.  Rows are the
+    // canonical (degree-major, lexicographic) positions; phi_m = prod x~[m_j]
+    // / sqrt(prod c!), x~ = x d^(-1/4).
     const float s4 = 1.0f / sqrtf(sqrtf((float)dk));
     const int npair = dk * (dk + 1) / 2;
-    const int64_t base2 = 1 + dk, base3 = 1 + dk + npair;
-    if (tid < npair) {
-      int i1 = 0, r = tid;
-      while (r >= dk - i1) {
-        r -= dk - i1;
-        ++i1;
+    const int base2 = 1 + dk, base3 = 1 + dk + npair;
+    int nitems = 0;
+    for (int m = dk; m > 0; m -= 8) nitems += m * (m + 1) / 2;
+    for (int it = tid; it < nitems; it += NTH) {
+      int h = 0, r = it;
+      for (int m = dk; r >= m * (m + 1) / 2; m -= 8) {
+        r -= m * (m + 1) / 2;
+        ++h;
       }
-      const int i2 = i1 + r;
+      int i2 = (int)((sqrtf(8.0f * (float)r + 1.0f) - 1.0f) * 0.5f);
+      while ((i2 + 1) * (i2 + 2) / 2 <= r) ++i2;
+      while (i2 * (i2 + 1) / 2 > r) --i2;
+      const int i1 = r - i2 * (i2 + 1) / 2;
       const float qa = xq[i1] * s4, qb = xq[i2] * s4, ka = xk[i1] * s4, kb = xk[i2] * s4;
-      const float w2 = (i1 == i2) ? 0.70710678118654752f : 1.0f;
-      fkq[base2 + tid] = float2{ka * kb * w2, qa * qb * w2};
-      // degree-3 tuples before (i1, i2, .): all with a smaller first index, then
-      // first index i1 and second index in [i1, i2)
-      const int64_t c3 = (int64_t)(dk + 2) * (dk + 1) * dk / 6 - (int64_t)(dk - i1 + 2) * (dk - i1 + 1) * (dk - i1) / 6;
-      const int64_t f3 = base3 + c3 + (int64_t)(i2 - i1) * dk - ((int64_t)i2 * (i2 - 1) - (int64_t)i1 * (i1 - 1)) / 2;
+      if (h == 0) {
+        const float w2 = (i1 == i2) ? 0.70710678118654752f : 1.0f;
+        fkq[base2 + i1 * dk - i1 * (i1 - 1) / 2 + (i2 - i1)] = float2{ka * kb * w2, qa * qb * w2};
+      }
+      // degree-3 tuples before (i1, i2, i2): all with a smaller first index,
+      // then first index i1 and second index in [i1, i2)
+      const int start3 = base3 + (dk + 2) * (dk + 1) * dk / 6 - (dk - i1 + 2) * (dk - i1 + 1) * (dk - i1) / 6 +
+                         (i2 - i1) * dk - (i2 * (i2 - 1) - i1 * (i1 - 1)) / 2;
       const float pq = qa * qb, pk = ka * kb;
-      for (int i3 = i2; i3 < dk; ++i3) {
+      const int j0 = i2 + 8 * h;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int i3 = j0 + u;
+        const int ic = min(i3, dk - 1);  // in range, so the reads need no guard
+        const float xk3 = xk[ic] * s4, xq3 = xq[ic] * s4;
         // 1 / sqrt(prod c!): 1/sqrt(6) for three equal indices, 1/sqrt(2) for two
         const float w3 = (i1 == i3) ? 0.40824829046386302f : ((i1 == i2 || i2 == i3) ? 0.70710678118654752f : 1.0f);
-        fkq[f3 + (i3 - i2)] = float2{pk * (xk[i3] * s4) * w3, pq * (xq[i3] * s4) * w3};
+        if (i3 < dk) fkq[start3 + (i3 - i2)] = float2{pk * xk3 * w3, pq * xq3 * w3};
       }
-    } else if (tid < npair + dk) {
-      const int i = tid - npair;
-      fkq[1 + i] = float2{xk[i] * s4, xq[i] * s4};
-    } else if (tid == npair + dk) {
-      fkq[0] = float2{1.0f, 1.0f};
     }
+    const int t1 = NTH - 1 - tid;
+    if (t1 == 0)
+      fkq[0] = float2{1.0f, 1.0f};
+    else if (t1 <= dk)
+      fkq[t1] = float2{xk[t1 - 1] * s4, xq[t1 - 1] * s4};
   } else {
     // the table entries of up to 8 features per thread are loaded together
     for (int64_t fb = tid; fb < D; fb += 8 * NTH) {
@@ -242,7 +283,7 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
       }
     }
   }
-  __syncthreads();
+  lds_barrier();
   if (lt >= 0 && lt < nleft) {
     const int64_t f = le / E;
     const int j = (int)(le - f * E);
@@ -266,19 +307,20 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
   }
   float4* const Sw = (float4*)(Sh + a0);
   if (active) {
-    for (int64_t m0 = 0;; m0 += kFlatUnroll) {
+    for (int64_t m0 = m_lo;; m0 += kFlatUnroll) {
       float4 nxt[kFlatUnroll];
 #pragma unroll
       for (int u = 0; u < kFlatUnroll; ++u) {
-        const int64_t g = tid + (int64_t)tu * (m0 + kFlatUnroll + u);
-        nxt[u] = (g < nv) ? Sv[g] : float4{0.0f, 0.0f, 0.0f, 0.0f};
+        const int64_t m = m0 + kFlatUnroll + u;
+        const int64_t g = tid + (int64_t)tu * m;
+        nxt[u] = (g < nv && m < m_hi) ? Sv[g] : float4{0.0f, 0.0f, 0.0f, 0.0f};
       }
       bool more = false;
 #pragma unroll
       for (int u = 0; u < kFlatUnroll; ++u) {
         const int64_t m = m0 + u;
         const int64_t g = tid + (int64_t)tu * m;
-        if (g < nv) {
+        if (g < nv && m < m_hi) {
           float x[4] = {cur[u].x, cur[u].y, cur[u].z, cur[u].w};
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
@@ -316,6 +358,20 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
   if (tid == 0)
     for (int i = 0; i < nleft; ++i) o[lo_col[i]] += lo_val[i];  // leftover terms, in element order
   __syncthreads();
+  if (split) {
+    if (tid < E)
+      __hip_atomic_store(xpart + (bh * 2 + piece) * E + tid, o[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __builtin_amdgcn_s_waitcnt(0);  // the stores have completed before the count goes up
+    __syncthreads();
+    int* const arrived = (int*)red;  // (the column sums are no longer needed)
+    if (tid == 0) arrived[0] = __hip_atomic_fetch_add(cnt + bh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    if (arrived[0] == 0) return;  // the other piece finishes the head
+    if (tid < E)
+      o[tid] += __hip_atomic_load(xpart + (bh * 2 + (piece ^ 1)) * E + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) __hip_atomic_store(cnt + bh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+  }
   for (int j = tid; j < dv; j += NTH) y[bh * dv + j] = from_f32<T>(o[j] / o[dv]);
 }
 
@@ -548,9 +604,13 @@ DecodePlan plan_decode(int64_t D, int dk, int dv) {
     const int unit = E / std::gcd(E, 4);
     const int tu = (nth / unit) * unit;
     const size_t lds = sizeof(float2) * (size_t)D + sizeof(float) * (size_t)(2 * dk + E + 4 * tu + 9 * E + 16);
-    if (tu > 0 && 8 * E <= nth && lds <= 150 * 1024) {
+    if (tu > 0 && 8 * E <= nth && dk < nth && lds <= 150 * 1024) {
       p.flat_tu = tu;
       p.flat_lds = lds;
+      // two pieces per head, the even-XCD one taking kFlatEvenShare of the
+      // steps; two such workgroups fit a CU (LDS, and 64 VGPRs each)
+      const int64_t steps = (D * E / 4 + tu - 1) / tu;
+      if (2 * lds <= 160 * 1024 && steps >= 4) p.flat_msplit = (int)(kFlatEvenShare * (double)steps + 0.5);
     }
     return p;
   }
@@ -566,17 +626,18 @@ DecodePlan plan_decode(int64_t D, int dk, int dv) {
 
 hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, void* y, bool bf16, int BH,
                          int dk, int dv, const DevTable& t, const DecodePlan& plan, float* partial,
-                         hipStream_t s) {
+                         int* counters, hipStream_t s) {
   const int E = dv + 1;
   if (plan.flat_tu > 0 && ((uintptr_t)S & 15) == 0) {
     hipError_t e;
+    const bool split = plan.flat_msplit > 0 && partial != nullptr && counters != nullptr;
 #define SATA_DECODE_FLAT(TT)                                                                              \
   e = hipFuncSetAttribute((const void*)decode_flat_kernel<TT, 1024>,                                      \
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)plan.flat_lds);                \
   if (e != hipSuccess) return e;                                                                          \
-  hipLaunchKernelGGL((decode_flat_kernel<TT, 1024>), dim3((unsigned)BH), dim3(1024), plan.flat_lds, s, S,  \
-                     (const TT*)q, (const TT*)k, (const TT*)v, (TT*)y, t.packed, t.weight, t.D, dk, dv,   \
-                     plan.flat_tu, t.P)
+  hipLaunchKernelGGL((decode_flat_kernel<TT, 1024>), dim3((unsigned)BH * (split ? 2u : 1u)), dim3(1024),        \
+                     plan.flat_lds, s, S, (const TT*)q, (const TT*)k, (const TT*)v, (TT*)y, t.packed, t.weight,   \
+                     t.D, dk, dv, plan.flat_tu, t.P, plan.flat_msplit, split ? partial : nullptr, counters)
     if (bf16) { SATA_DECODE_FLAT(bf16_t); } else { SATA_DECODE_FLAT(float); }
 #undef SATA_DECODE_FLAT
     return hipGetLastError();

@@ -54,6 +54,7 @@ struct Workspace {
 struct DeviceCache {
   std::map<std::pair<int, int>, TableEntry> tables;
   std::map<hipStream_t, Workspace> workspaces;
+  std::map<hipStream_t, Workspace> counters;  // zeroed at allocation; kernels leave them zero
 };
 
 std::mutex g_mu;
@@ -123,6 +124,36 @@ sata_status get_workspace(size_t bytes, hipStream_t stream, void** out) {
     ws.bytes = want;
   }
   *out = ws.ptr;
+  return SATA_OK;
+}
+
+// Returns a per-(device, stream) array of at least n ints, all zero.  It is
+// cleared once, when allocated, by a fill kernel on the stream; the kernels
+// that count in it set every counter back to zero.
+sata_status get_counters(int64_t n, hipStream_t stream, int** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lock(g_mu);
+  Workspace& ws = g_devices[dev].counters[stream];
+  const size_t bytes = sizeof(int) * (size_t)n;
+  if (ws.bytes < bytes) {
+    if (ws.ptr) {
+      if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+      hipFree(ws.ptr);
+      ws.ptr = nullptr;
+      ws.bytes = 0;
+    }
+    size_t want = bytes < ((size_t)1 << 16) ? ((size_t)1 << 16) : bytes;
+    if ((e = hipMalloc(&ws.ptr, want)) != hipSuccess) return hip_fail(e, "hipMalloc(counters)");
+    if ((e = sata::launch_fill_zero((float*)ws.ptr, (int64_t)(want / sizeof(float)), stream)) != hipSuccess) {
+      hipFree(ws.ptr);
+      ws.ptr = nullptr;
+      return hip_fail(e, "clearing counters");
+    }
+    ws.bytes = want;
+  }
+  *out = (int*)ws.ptr;
   return SATA_OK;
 }
 
@@ -274,13 +305,18 @@ sata_status sata_decode_step(float* S, const void* q, const void* k, const void*
   if ((st = get_table(d_k, P, s, &t)) != SATA_OK) return st;
   sata::DecodePlan plan = sata::plan_decode(D, d_k, d_v);
   float* partial = nullptr;
-  if (plan.nslices > 1) {
+  int* counters = nullptr;
+  // partial sums: one row per slice, or per piece of a head split in two
+  const int64_t rows = (plan.nslices > 1) ? plan.nslices : (plan.flat_msplit > 0 ? 2 : 0);
+  if (rows > 0) {
     void* ws = nullptr;
-    const size_t bytes = sizeof(float) * (size_t)BH * plan.nslices * (d_v + 1);
+    const size_t bytes = sizeof(float) * (size_t)BH * rows * (d_v + 1);
     if ((st = get_workspace(bytes, s, &ws)) != SATA_OK) return st;
     partial = (float*)ws;
   }
-  hipError_t e = sata::launch_decode(S, q, k, v, y, dt == SATA_BF16, BH, d_k, d_v, t, plan, partial, s);
+  if (plan.flat_msplit > 0 && (st = get_counters(BH, s, &counters)) != SATA_OK) return st;
+  hipError_t e =
+      sata::launch_decode(S, q, k, v, y, dt == SATA_BF16, BH, d_k, d_v, t, plan, partial, counters, s);
   if (e != hipSuccess) return hip_fail(e, "decode launch");
   return ok();
 }
@@ -309,6 +345,7 @@ void sata_release(void) {
       hipFree(t.second.weight);
     }
     for (auto& w : kv.second.workspaces) hipFree(w.second.ptr);
+    for (auto& w : kv.second.counters) hipFree(w.second.ptr);
   }
   g_devices.clear();
   hipSetDevice(cur);
