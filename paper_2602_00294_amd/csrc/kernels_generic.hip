@@ -165,7 +165,7 @@ template <typename T, int NTH>
 __global__ void __launch_bounds__(NTH, 8)
 decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __restrict__ k,
                    const T* __restrict__ v, T* __restrict__ y, const uint64_t* __restrict__ packed,
-                   const float* __restrict__ weight, int64_t D, int dk, int dv, int tu, int P,
+                   const float* __restrict__ weight, int64_t D, int dk, int dv, int tu, int P, float xscale,
                    int msplit, float* __restrict__ xpart, int* __restrict__ cnt) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
   const int E = dv + 1;
@@ -191,17 +191,24 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
   const int64_t nv = (N - a0) / 4;         // float4s in the aligned part
   const float4* const Sv = (const float4*)(Sh + a0);
   const bool active = tid < tu;
-  // leftover elements [0, a0) and [a0 + 4 nv, N): one per thread of the last wave
-  const int nlead = (int)min<int64_t>(a0, N);
-  const int nleft = piece ? 0 : nlead + (int)(N - (a0 + 4 * nv));
+  // leftover elements [0, a0) and [a0 + 4 nv, N): one per thread of the last
+  // wave; a split head's first piece takes the leading ones, its second the
+  // trailing ones
+  const int nlead = (split && piece == 1) ? 0 : (int)min<int64_t>(a0, N);
+  const int ntrail = (split && piece == 0) ? 0 : (int)(N - (a0 + 4 * nv));
+  const int nleft = nlead + ntrail;
   const int lt = tid - (NTH - 8);
   const int64_t le = (lt < nlead) ? lt : a0 + 4 * nv + (lt - nlead);
+  // the state rows this workgroup touches (a split piece needs only its own)
+  const int64_t e_split = a0 + 4 * min<int64_t>(nv, (int64_t)tu * msplit);
+  const int64_t row_lo = (split && piece == 1) ? min<int64_t>(D - 1, e_split / E) : 0;
+  const int64_t row_hi = (split && piece == 0) ? (e_split - 1) / E : D - 1;
   // q, k, v go to LDS first (in the first wave, which waits for them there),
   // then every wave sends its first state loads, which stay in flight while
   // the features are computed: the barriers below wait for LDS only
   if (tid < dk) {
-    xq[tid] = to_f32(q[bh * dk + tid]);
-    xk[tid] = to_f32(k[bh * dk + tid]);
+    xq[tid] = to_f32(q[bh * dk + tid]) * xscale;
+    xk[tid] = to_f32(k[bh * dk + tid]) * xscale;
   }
   if (tid < E) ve[tid] = (tid < dv) ? to_f32(v[bh * dv + tid]) : 1.0f;
   // (branch-free: an out-of-range slot reads element 0, which the stream skips)
@@ -216,15 +223,15 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
   lx = lead ? lx : 0.0f;
   lds_barrier();
   if (P == 4) {
-    // Features in closed form, no table.  Work items are (prefix i1 <= i2,
-    // block h of up to 8 third indices i3 in [i2 + 8h, i2 + 8h + 8)); tier h
-    // holds the prefixes with i2 < d - 8h, numbered i2-major (rank
-    // i2 (i2 + 1) / 2 + i1), so a thread's item decodes without a search
-    // and none walks more than 8 features.  Tier 0 also writes the degree-2
-    // feature (i1, i2); the last threads write degrees 0 and 1.  Rows are the
-    // canonical (degree-major, lexicographic) positions; phi_m = prod x~[m_j]
-    // / sqrt(prod c!), x~ = x d^(-1/4).
-    const float s4 = 1.0f / sqrtf(sqrtf((float)dk));
+    // Features in closed form, no table (LDS holds x~ = x d^(-1/4)).  Work
+    // items are (prefix i1 <= i2, block h of up to 8 third indices i3 in
+    // [i2 + 8h, i2 + 8h + 8)); tier h holds the prefixes with i2 < d - 8h,
+    // numbered i2-major (rank i2 (i2 + 1) / 2 + i1), so an item decodes
+    // without a search and none walks more than 8 features.  Tier 0 also
+    // writes the degree-2 feature (i1, i2); the last threads write degrees 0
+    // and 1.  Rows are the canonical (degree-major, lexicographic) positions;
+    // phi_m = prod x~[m_j] / sqrt(prod c!).  Items wholly outside this
+    // workgroup's rows are skipped.
     const int npair = dk * (dk + 1) / 2;
     const int base2 = 1 + dk, base3 = 1 + dk + npair;
     int nitems = 0;
@@ -235,28 +242,35 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
         r -= m * (m + 1) / 2;
         ++h;
       }
-      int i2 = (int)((sqrtf(8.0f * (float)r + 1.0f) - 1.0f) * 0.5f);
+      // i2 = floor((sqrt(8 r + 1) - 1) / 2), from an estimate and exact corrections
+      int i2 = (int)((__builtin_amdgcn_sqrtf(8.0f * (float)r + 1.0f) - 1.0f) * 0.5f);
       while ((i2 + 1) * (i2 + 2) / 2 <= r) ++i2;
       while (i2 * (i2 + 1) / 2 > r) --i2;
       const int i1 = r - i2 * (i2 + 1) / 2;
-      const float qa = xq[i1] * s4, qb = xq[i2] * s4, ka = xk[i1] * s4, kb = xk[i2] * s4;
+      const float qa = xq[i1], qb = xq[i2], ka = xk[i1], kb = xk[i2];
       if (h == 0) {
+        const int row2 = base2 + i1 * dk - i1 * (i1 - 1) / 2 + (i2 - i1);
         const float w2 = (i1 == i2) ? 0.70710678118654752f : 1.0f;
-        fkq[base2 + i1 * dk - i1 * (i1 - 1) / 2 + (i2 - i1)] = float2{ka * kb * w2, qa * qb * w2};
+        if (row2 >= row_lo && row2 <= row_hi) fkq[row2] = float2{ka * kb * w2, qa * qb * w2};
       }
       // degree-3 tuples before (i1, i2, i2): all with a smaller first index,
       // then first index i1 and second index in [i1, i2)
       const int start3 = base3 + (dk + 2) * (dk + 1) * dk / 6 - (dk - i1 + 2) * (dk - i1 + 1) * (dk - i1) / 6 +
                          (i2 - i1) * dk - (i2 * (i2 - 1) - i1 * (i1 - 1)) / 2;
-      const float pq = qa * qb, pk = ka * kb;
       const int j0 = i2 + 8 * h;
+      const int64_t rfirst = start3 + (j0 - i2);
+      if (rfirst > row_hi || rfirst + 7 < row_lo) continue;
+      const float pq = qa * qb, pk = ka * kb;
+      // 1 / sqrt(prod c!): three equal indices (1/sqrt(6)) only at i3 = i2 = i1,
+      // two (1/sqrt(2)) at i3 = i2 or i1 = i2
+      const float wrest = (i1 == i2) ? 0.70710678118654752f : 1.0f;
+      const float wfirst = (h > 0) ? wrest : ((i1 == i2) ? 0.40824829046386302f : 0.70710678118654752f);
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int i3 = j0 + u;
         const int ic = min(i3, dk - 1);  // in range, so the reads need no guard
-        const float xk3 = xk[ic] * s4, xq3 = xq[ic] * s4;
-        // 1 / sqrt(prod c!): 1/sqrt(6) for three equal indices, 1/sqrt(2) for two
-        const float w3 = (i1 == i3) ? 0.40824829046386302f : ((i1 == i2 || i2 == i3) ? 0.70710678118654752f : 1.0f);
+        const float xk3 = xk[ic], xq3 = xq[ic];
+        const float w3 = (u == 0) ? wfirst : wrest;
         if (i3 < dk) fkq[start3 + (i3 - i2)] = float2{pk * xk3 * w3, pq * xq3 * w3};
       }
     }
@@ -264,7 +278,7 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
     if (t1 == 0)
       fkq[0] = float2{1.0f, 1.0f};
     else if (t1 <= dk)
-      fkq[t1] = float2{xk[t1 - 1] * s4, xq[t1 - 1] * s4};
+      fkq[t1] = float2{xk[t1 - 1], xq[t1 - 1]};
   } else {
     // the table entries of up to 8 features per thread are loaded together
     for (int64_t fb = tid; fb < D; fb += 8 * NTH) {
@@ -631,13 +645,16 @@ hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, 
   if (plan.flat_tu > 0 && ((uintptr_t)S & 15) == 0) {
     hipError_t e;
     const bool split = plan.flat_msplit > 0 && partial != nullptr && counters != nullptr;
+    // x d^(-1/4) for the closed-form P = 4 features (the float operations the
+    // features would otherwise do per use); the table path scales by itself
+    const float xscale = (t.P == 4) ? 1.0f / std::sqrt(std::sqrt((float)dk)) : 1.0f;
 #define SATA_DECODE_FLAT(TT)                                                                              \
   e = hipFuncSetAttribute((const void*)decode_flat_kernel<TT, 1024>,                                      \
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)plan.flat_lds);                \
   if (e != hipSuccess) return e;                                                                          \
   hipLaunchKernelGGL((decode_flat_kernel<TT, 1024>), dim3((unsigned)BH * (split ? 2u : 1u)), dim3(1024),        \
                      plan.flat_lds, s, S, (const TT*)q, (const TT*)k, (const TT*)v, (TT*)y, t.packed, t.weight,   \
-                     t.D, dk, dv, plan.flat_tu, t.P, plan.flat_msplit, split ? partial : nullptr, counters)
+                     t.D, dk, dv, plan.flat_tu, t.P, xscale, plan.flat_msplit, split ? partial : nullptr, counters)
     if (bf16) { SATA_DECODE_FLAT(bf16_t); } else { SATA_DECODE_FLAT(float); }
 #undef SATA_DECODE_FLAT
     return hipGetLastError();
