@@ -489,25 +489,27 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
         // slot p's MFMAs run, and a new run's B is built behind them.
         bf16x8 Bk[4];
         auto build_b = [&](uint32_t m, bf16x8 (&Bk)[4]) __attribute__((always_inline)) {
+          // one uniform branch on the kind, so that each case is a single block
+          // whose LDS reads the scheduler can issue together
           const uint32_t kind = s_kind(m);
+          if (kind == kTop) {
+            const float* kr = kt + s_i1(m) * kTS + 8 * qh;
+            const float* vr = vt + l31 * kTS + 8 * qh;
 #pragma unroll
-          for (int s = 0; s < 4; ++s) {
-            const int tk = 16 * s + 8 * qh;
-            if (kind == kTop) {
-              const float* kr = kt + s_i1(m) * kTS + tk;
-              const float* vr = vt + l31 * kTS + tk;
-              const float4 k0 = *(const float4*)kr, k1 = *(const float4*)(kr + 4);
-              const float4 v0 = *(const float4*)vr, v1 = *(const float4*)(vr + 4);
+            for (int s = 0; s < 4; ++s) {
+              const float4 k0 = *(const float4*)(kr + 16 * s), k1 = *(const float4*)(kr + 16 * s + 4);
+              const float4 v0 = *(const float4*)(vr + 16 * s), v1 = *(const float4*)(vr + 16 * s + 4);
               uint4 w;
               w.x = pack2(k0.x * v0.x, k0.y * v0.y);
               w.y = pack2(k0.z * v0.z, k0.w * v0.w);
               w.z = pack2(k1.x * v1.x, k1.y * v1.y);
               w.w = pack2(k1.z * v1.z, k1.w * v1.w);
               Bk[s] = __builtin_bit_cast(bf16x8, w);
-            } else {
-              const u16* src = (kind == kLow) ? vtb : ktb;
-              Bk[s] = __builtin_bit_cast(bf16x8, *(const uint4*)(src + l31 * kTSb + tk));
             }
+          } else {
+            const u16* src = ((kind == kLow) ? vtb : ktb) + l31 * kTSb + 8 * qh;
+#pragma unroll
+            for (int s = 0; s < 4; ++s) Bk[s] = __builtin_bit_cast(bf16x8, *(const uint4*)(src + 16 * s));
           }
         };
         auto load_a = [&](uint32_t m, bf16x8 (&A)[4]) __attribute__((always_inline)) {
@@ -658,36 +660,52 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
           if (m & kLast) {
             // run epilogue into this SIMD's sums: scale by q~[:, i1] (TOP), 1
             // (LOW) or contract with q~ (ZMAT).  Each lane owns its entries.
+            // (uniform branches on the kind outside the tile loops, so that each
+            // case is one block whose LDS accesses can be issued together)
             const uint32_t kind = s_kind(m);
+            if (kind == kZmat) {
 #pragma unroll
-            for (int t = 0; t < 2; ++t) {
-              const float* qrow = xq + (32 * t + l31) * kXS;
-              float* rr = pr + (32 * t + l31) * EP;
-              if (kind == kZmat) {
+              for (int t = 0; t < 2; ++t) {
+                const float* qrow = xq + (32 * t + l31) * kXS;
                 float z = 0.0f;
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
                   const float4 w = *(const float4*)(qrow + 8 * g + 4 * qh);
                   z += w.x * R[t][4 * g + 0] + w.y * R[t][4 * g + 1] + w.z * R[t][4 * g + 2] + w.w * R[t][4 * g + 3];
                 }
-                rr[DV + qh] += z;
-              } else if (!(m & kEmpty)) {
-                const float sc = (kind == kTop) ? qrow[s_i1(m)] : 1.0f;
+                pr[(32 * t + l31) * EP + DV + qh] += z;
+              }
+            } else if (!(m & kEmpty)) {
+              // q~[:, i1] is read for LOW runs too (i1 = 0) and replaced by 1,
+              // so that no branch splits the reads; each tile's sums are read
+              // together, updated, then written
+              const bool top = kind == kTop;
+              const int i1 = s_i1(m);
+              float sc[2];
+#pragma unroll
+              for (int t = 0; t < 2; ++t) sc[t] = xq[(32 * t + l31) * kXS + i1];
+#pragma unroll
+              for (int t = 0; t < 2; ++t) {
+                const float f = top ? sc[t] : 1.0f;
+                float4* o = (float4*)(pr + (32 * t + l31) * EP + 4 * qh);
+                float4 cur[4];
+#pragma unroll
+                for (int g = 0; g < 4; ++g) cur[g] = o[2 * g];
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
-                  float4* o = (float4*)(rr + 8 * g + 4 * qh);
-                  float4 cur = *o;
-                  cur.x += sc * R[t][4 * g + 0];
-                  cur.y += sc * R[t][4 * g + 1];
-                  cur.z += sc * R[t][4 * g + 2];
-                  cur.w += sc * R[t][4 * g + 3];
-                  *o = cur;
+                  cur[g].x += f * R[t][4 * g + 0];
+                  cur[g].y += f * R[t][4 * g + 1];
+                  cur[g].z += f * R[t][4 * g + 2];
+                  cur[g].w += f * R[t][4 * g + 3];
                 }
+#pragma unroll
+                for (int g = 0; g < 4; ++g) o[2 * g] = cur[g];
               }
-              // restart the sums on the matrix core (a zero product) instead
-              // of 16 vector moves
-              R[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(zop, zop, f32x16{}, 0, 0, 0);
             }
+            // restart the sums on the matrix core (a zero product) instead of
+            // 16 vector moves
+#pragma unroll
+            for (int t = 0; t < 2; ++t) R[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(zop, zop, f32x16{}, 0, 0, 0);
           }
           if (p + 1 < PPW) {
             convert(S[p + 1 < PPW ? p + 1 : p], M(p + 1 < PPW ? p + 1 : p), fw, An);
