@@ -189,13 +189,35 @@ constexpr int kXS = 36;  // floats per token row of the staged x~ tiles
 constexpr int kPS = 36;  // floats per token row of the per-SIMD sums and of the slice partials
                          // (value columns, then the normaliser; 16-byte aligned rows)
 
+// A unit whose 8 features are all degree 0 or padding holds the same values
+// for every token and chunk: it is written once, not generated.
+template <int DK, int U>
+__host__ __device__ constexpr bool unit_const() {
+  for (int i = 0; i < 8; ++i)
+    if (low_feat<DK>(32 * (U / 4) + swap23(8 * (U % 4) + i)).deg > 0) return false;
+  return true;
+}
+template <int DK, int U, int NU>
+__device__ __forceinline__ void put_const_units(char* row, int ulo, int uhi, int sw16) {
+  if constexpr (U < NU) {
+    if constexpr (unit_const<DK, U>()) {
+      if (U >= ulo && U < uhi) {
+        const float x0[DK] = {};
+        *(uint4*)(row + 64 * (U / 4) + ((16 * (U % 4)) ^ sw16)) = gen_unit<DK, U>(x0);
+      }
+    }
+    put_const_units<DK, U + 1, NU>(row, ulo, uhi, sw16);
+  }
+}
+
 // Generation units of one wave: absolute units U = W, W + kNW, ... inside the
-// slice's range [ulo, uhi).  row points at this lane's token row shifted back
+// slice's range [ulo, uhi), constant units excepted.  row points at this lane's token row shifted back
 // by the slice's first column group; sw16 = 16 ((t / 4) % 4).
 template <int DK, int U, int NU>
 __device__ __forceinline__ void gen_chain(const float (&x)[DK], int ulo, int uhi, char* row, int sw16) {
   if constexpr (U < NU) {
-    if (U >= ulo && U < uhi) *(uint4*)(row + 64 * (U / 4) + ((16 * (U % 4)) ^ sw16)) = gen_unit<DK, U>(x);
+    if constexpr (!unit_const<DK, U>())
+      if (U >= ulo && U < uhi) *(uint4*)(row + 64 * (U / 4) + ((16 * (U % 4)) ^ sw16)) = gen_unit<DK, U>(x);
     gen_chain<DK, U + kNW, NU>(x, ulo, uhi, row, sw16);
   }
 }
@@ -204,7 +226,8 @@ __device__ __forceinline__ void gen_chain(const float (&x)[DK], int ulo, int uhi
 template <int DK, int U, int NU, int ULO, int UHI>
 __device__ __forceinline__ void gen_chain_ct(const float (&x)[DK], char* row, int sw16) {
   if constexpr (U < NU) {
-    if constexpr (U >= ULO && U < UHI) *(uint4*)(row + 64 * (U / 4) + ((16 * (U % 4)) ^ sw16)) = gen_unit<DK, U>(x);
+    if constexpr (U >= ULO && U < UHI && !unit_const<DK, U>())
+      *(uint4*)(row + 64 * (U / 4) + ((16 * (U % 4)) ^ sw16)) = gen_unit<DK, U>(x);
     gen_chain_ct<DK, U + kNW, NU, ULO, UHI>(x, row, sw16);
   }
 }
@@ -303,6 +326,11 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
   // and the partial regions
   for (int i = tid; i < kC * kPhiStride / 16; i += kNW * 64) ((uint4*)phik)[i] = uint4{0u, 0u, 0u, 0u};
   for (int i = tid; i < (L::RQ - L::KT) / 16; i += kNW * 64) ((uint4*)(smem + L::KT))[i] = uint4{0u, 0u, 0u, 0u};
+  __syncthreads();
+  // the constant feature units of both phi tiles (waves 0 and 1: one token row per lane)
+  if (wave < 2)
+    put_const_units<DK, 0, NU>((wave == 0 ? phiq : phik) + lane_id * kPhiStride - 64 * lo, 4 * lo, 4 * (lo + nc),
+                               16 * ((lane_id >> 2) & 3));
 
   f32x16 S[PPW];
 #pragma unroll
@@ -348,8 +376,8 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
       const int tok = pc / (DK / 8);
       const int g = c * kC + tok;
       uint4 r = {0u, 0u, 0u, 0u};
-      if (lid < 32 && pc < kC * DK / 8 && c < nch && g < n)
-        r = *(const uint4*)(base + (int64_t)g * DK + (pc - tok * (DK / 8)) * 8);
+      const u16* const cb = base + (int64_t)c * kC * DK;  // wave-uniform
+      if (lid < 32 && pc < kC * DK / 8 && c < nch && g < n) r = *(const uint4*)(cb + (tok * DK + (pc - tok * (DK / 8)) * 8));
       return r;
     };
     auto store_piece = [&](int tile_off, int lid, uint4 w) __attribute__((always_inline)) {
@@ -443,29 +471,40 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
           // the four per-SIMD readout sums of chunk c -> this slice's partial
           // (rows of kPS floats: 32 values, the normaliser), clearing them; 8
           // threads per token, 4 value columns each, the first also the normaliser
-          const int tok = tid >> 3;
-          const int cq = 4 * (tid & 7);
+          // (every lane reads its token's normaliser pair, so that no branch
+          // splits the reads; the first lane of the token uses and clears it)
+          // (from a laundered thread index, so these offsets are formed here
+          // each iteration rather than kept, or spilled, across the loop)
+          int ftid = tid;
+          asm volatile("" : "+v"(ftid));
+          const int tok = ftid >> 3;
+          const int cq = 4 * (ftid & 7);
+          float4 w[4];
+          float2 zz[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float* pr = part + (r * kC + tok) * EP;
+            w[r] = *(const float4*)(pr + cq);
+            zz[r] = *(const float2*)(pr + DV);
+          }
           float4 o = {0.0f, 0.0f, 0.0f, 0.0f};
           float z = 0.0f;
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             float* pr = part + (r * kC + tok) * EP;
-            const float4 w = *(const float4*)(pr + cq);
-            o.x += w.x;
-            o.y += w.y;
-            o.z += w.z;
-            o.w += w.w;
+            o.x += w[r].x;
+            o.y += w[r].y;
+            o.z += w[r].z;
+            o.w += w[r].w;
+            z += zz[r].x + zz[r].y;
             *(float4*)(pr + cq) = float4{0.0f, 0.0f, 0.0f, 0.0f};
-            if (cq == 0) {
-              const float2 zz = *(const float2*)(pr + DV);
-              z += zz.x + zz.y;
-              *(float2*)(pr + DV) = float2{0.0f, 0.0f};
-            }
+            if (cq == 0) *(float2*)(pr + DV) = float2{0.0f, 0.0f};
           }
           if (tok < cn) {
-            float* dst = partial + ((((int64_t)slice * BH + bh) * n + t0 + tok) * kPS);
-            *(float4*)(dst + cq) = o;
-            if (cq == 0) dst[DV] = z;
+            // a wave-uniform row base and a 32-bit lane offset
+            float* const dst = partial + (((int64_t)slice * BH + bh) * n + t0) * kPS;
+            *(float4*)(dst + (tok * kPS + cq)) = o;
+            if (cq == 0) dst[tok * kPS + DV] = z;
           }
         }
         // (the flush first: its LDS reads then do not queue behind the feature
