@@ -685,17 +685,17 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
 #pragma unroll
         for (int p = 0; p < PPW; ++p) {
           const uint32_t m = M(p);
+          // the next slot's row factors are read before this slot's MFMAs, so
+          // that its conversion does not wait for them
+          float4 fw[4];
+          if (p + 1 < PPW) load_fac(M(p + 1 < PPW ? p + 1 : p), fw);
           R[0] = mfma32(Ac[0], __builtin_bit_cast(bf16x8, bc[0]), R[0]);
           R[0] = mfma32(Ac[1], __builtin_bit_cast(bf16x8, bc[1]), R[0]);
           R[1] = mfma32(Ac[0], __builtin_bit_cast(bf16x8, bc[2]), R[1]);
           R[1] = mfma32(Ac[1], __builtin_bit_cast(bf16x8, bc[3]), R[1]);
           uint4 bn[4];
-          float4 fw[4];
           bf16x8 An[2];
-          if (p + 1 < PPW) {
-            load_b(M(p + 1), bn);
-            load_fac(M(p + 1), fw);
-          }
+          if (p + 1 < PPW) load_b(M(p + 1), bn);
           if (m & kLast) {
             // run epilogue into this SIMD's sums: scale by q~[:, i1] (TOP), 1
             // (LOW) or contract with q~ (ZMAT).  Each lane owns its entries.
