@@ -11,9 +11,20 @@ tokens per step divided by the step time; the prefill and decode rates are
 reported separately next to it.  `roofline` is for the kernel that takes the
 largest share of the step (`rooflines` lists both); its achieved rate is the
 algorithmic work of one launch divided by the launch's average duration,
-measured with HIP events on the stream the kernels run on.
+measured with HIP events on the stream the kernels run on.  The CPU baseline
+leg times the float64 oracle on a sample of the same workload and also checks
+the timed GPU output against it on a few rows.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--decode-steps M] [--no-cpu-baseline]
+
+`--workload` selects one of the other workload shapes instead, each printing
+its own line in the same form:
+  decode_d16  B=64, H=32, d_k=d_v=16, P=4, bf16: 2048-token prefill, then 4096
+              decode steps (the decode figure is the one that counts);
+  large_d64   B=2, H=8, d_k=d_v=64, P=4 (D=47905), bf16: 4096-token prefill,
+              then 1024 decode steps;
+  sweep_d16   B=1, H=64, d_k=d_v=16, float32, n=65536: prefill for each P in
+              2..6 (the CPU leg also reports the error against softmax).
 """
 from __future__ import annotations
 
@@ -30,6 +41,8 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
+# float32 vector peak (packed FMA counted): the bound of the float32 prefill path
+PEAK_F32_TFLOPS = 157.3
 
 WORKLOAD_ID = 3
 B, H, N, DK, DV, P, CHUNK = 8, 32, 8192, 32, 32, 4, 64
@@ -88,6 +101,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-heads", type=int, default=48)
     ap.add_argument("--cpu-sample-decode-rows", type=int, default=128)
+    ap.add_argument("--workload", default="headline", choices=["headline", "decode_d16", "large_d64", "sweep_d16"])
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before timing, run one device-to-device copy of this many MiB (a kernel of "
                          "known traffic for calibrating hardware byte counters)")
@@ -117,8 +131,10 @@ def make_inputs(dec_steps):
     return pre, dec
 
 
-def cpu_baseline(n_heads, dec_rows):
-    """Times the float64 oracle on a bounded sample of the same workload."""
+def cpu_baseline(n_heads, dec_rows, y_gpu=None):
+    """Times the float64 oracle on a bounded sample of the same workload, and
+    checks the GPU prefill output y_gpu ([B, H, n, d_v] on the host) against it
+    on a few rows of the first and last head."""
     import numpy as np
 
     import oracle
@@ -141,6 +157,14 @@ def cpu_baseline(n_heads, dec_rows):
     # seconds per head-token, scaled to tokens of the whole batch (H heads per token)
     pre_tok_s = (len(heads) * N) / t_pre / H
     dec_tok_s = (len(heads) * dec_rows) / t_dec / H
+    parity = {}
+    if y_gpu is not None:
+        for (b, h) in ((0, 0), (B - 1, H - 1)):
+            q, k, v = syn.make_head(WORKLOAD_ID, b, h, N, DK, DV, "bf16")
+            rows = [0, 63, 64, 4095, N - 1]
+            yr, _, kap = oracle.taylor_attention_rows(q, k, v, P, rows)
+            err, _ = oracle.max_row_rel_error(y_gpu[b, h, rows], yr, kap)
+            parity[f"b{b}h{h}"] = err
     return {
         "value": None, "unit": "tokens/s", "cores": threads, "kind": "oracle",
         "prefill_tokens_per_s": pre_tok_s, "decode_tokens_per_s": dec_tok_s,
@@ -149,7 +173,143 @@ def cpu_baseline(n_heads, dec_rows):
                    f"rates scaled to whole-batch tokens (1 token = {H} head-tokens); decode rows near "
                    f"position {N} stand in for all {B}x{H} decode rows"),
         "seconds": t_pre + t_dec,
+        "parity_max_row_rel_err": parity,
     }
+
+
+WORKLOADS = {
+    # name: (synthetic stream id, B, H, prefill n, d, P values, dtype, decode steps)
+    "decode_d16": (2, 64, 32, 2048, 16, [4], "bf16", 4096),
+    "large_d64": (4, 2, 8, 4096, 64, [4], "bf16", 1024),
+    "sweep_d16": (5, 1, 64, 65536, 16, [2, 3, 4, 5, 6], "f32", 0),
+}
+
+
+def run_workload(args, sata, torch):
+    """One of the other workload shapes: prefill (per P) and decode, timed like
+    the headline; returns the JSON line."""
+    import numpy as np
+
+    import sata_synth as syn
+    wid, Bw, Hw, n, d, Ps, dt, n_dec = WORKLOADS[args.workload]
+    n_dec = n_dec if args.decode_steps == 1024 else args.decode_steps
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    ebytes = 2 if dt == "bf16" else 4
+    q = np.empty((Bw, Hw, n + n_dec, d), np.float32)
+    k, v = np.empty_like(q), np.empty_like(q)
+    for b in range(Bw):
+        for h in range(Hw):
+            q[b, h], k[b, h], v[b, h] = syn.make_head(wid, b, h, n + n_dec, d, d, dt)
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(tdt)
+    pre = [up(a[:, :, :n]) for a in (q, k, v)]
+    dec = [up(a[:, :, n:].transpose(2, 0, 1, 3)) for a in (q, k, v)]
+    del q, k, v
+    y = torch.empty(Bw, Hw, n, d, dtype=tdt, device="cuda")
+    ydec = torch.empty(max(n_dec, 1), Bw, Hw, d, dtype=tdt, device="cuda")
+    per_P = {}
+    t_total = 0.0
+    roof_pre = roof_dec = None
+    for Pw in Ps:
+        D = feature_count(d, Pw)
+        S = torch.empty(Bw, Hw, D, d + 1, dtype=torch.float32, device="cuda")
+
+        def step(ev):
+            ev[0].record()
+            sata.prefill(*pre, Pw, CHUNK, y=y, S=S)
+            ev[1].record()
+            for t in range(n_dec):
+                sata.decode_step(S, dec[0][t], dec[1][t], dec[2][t], Pw, y=ydec[t])
+            ev[2].record()
+        for _ in range(args.warmup):
+            step([torch.cuda.Event(enable_timing=True) for _ in range(3)])
+        torch.cuda.synchronize()
+        events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+        for s_ in range(args.steps):
+            step(events[s_])
+        torch.cuda.synchronize()
+        pre_ms = sum(e[0].elapsed_time(e[1]) for e in events) / args.steps
+        dec_ms = sum(e[1].elapsed_time(e[2]) for e in events) / args.steps if n_dec else 0.0
+        t_total += pre_ms + dec_ms
+        flops = prefill_flops_per_head_token(d, d, Pw, CHUNK) * Bw * Hw * n
+        mfma = dt == "bf16" and Pw == 4 and d in (16, 32)  # the matrix-core prefill shapes
+        peak = PEAK_BF16_TFLOPS if mfma else PEAK_F32_TFLOPS
+        ach = flops / (pre_ms * 1e-3) / 1e12
+        roof_pre = {"kernel": "sata_prefill (all launches of one call)", "bound": "mfma" if mfma else "alu",
+                    "achieved": ach, "peak": peak, "unit": "TFLOP/s", "frac": ach / peak, "traffic": None,
+                    "work_per_launch": flops}
+        entry = {"prefill_ms": pre_ms, "prefill_tokens_per_s": Bw * n / (pre_ms * 1e-3), "prefill_roofline": roof_pre}
+        if n_dec:
+            dbytes = decode_bytes_per_head_step(d, d, Pw, ebytes) * Bw * Hw
+            dach = dbytes / (dec_ms * 1e-3 / n_dec) / 1e9
+            roof_dec = {"kernel": "sata_decode_step (all launches of one call)", "bound": "hbm", "achieved": dach,
+                        "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": dach / PEAK_HBM_GBS, "traffic": None,
+                        "work_per_launch": dbytes}
+            entry.update({"decode_ms_per_step": dec_ms / n_dec, "decode_tokens_per_s": Bw * n_dec / (dec_ms * 1e-3),
+                          "decode_roofline": roof_dec})
+        per_P[str(Pw)] = entry
+        del S
+    tokens = Bw * (n + n_dec) * len(Ps)
+    line = {
+        "metric": "prefill tokens/s + decode tokens/s (d_k=32,P=4); % MFMA/HBM roofline",
+        "value": tokens / (t_total * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": t_total, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": dt, "data": "synthetic",
+        "config": {"workload": (f"{args.workload}: causal prefill B={Bw} H={Hw} n={n} d_k=d_v={d} "
+                                f"P={'/'.join(map(str, Ps))} {dt} chunk={CHUNK}"
+                                + (f" then {n_dec} decode steps" if n_dec else "")),
+                   "global_batch": Bw, "seq_len": n, "decode_steps": n_dec, "heads": Hw, "d_k": d, "d_v": d,
+                   "P": Ps if len(Ps) > 1 else Ps[0], "chunk": CHUNK, "parallelism": "single GPU"},
+        "per_P": per_P,
+        "roofline": roof_dec if roof_dec is not None else roof_pre,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline_workload(wid, Bw, Hw, n, d, Ps, dt, y if len(Ps) == 1 else None,
+                                                     pre if len(Ps) > 1 else None, sata, torch)
+    return line
+
+
+def cpu_baseline_workload(wid, Bw, Hw, n, d, Ps, dt, y_gpu, pre, sata, torch):
+    """The oracle on two heads of the workload: its rate on a bounded row sample,
+    the GPU output's error against it on those rows and, for the sweep, the
+    error of the P-term method against exact softmax attention per P."""
+    import numpy as np
+
+    import oracle
+    import sata_synth as syn
+    threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    heads = [(0, 0), (Bw - 1, Hw - 1)]
+    rows = sorted({0, 63, 64, n // 2, n - 1} | set(range(n - 96, n, 8)))
+    out = {"value": None, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+           "sample": f"rows {rows[0]}..{rows[-1]} ({len(rows)} rows) of heads {heads}, direct float64 definition"}
+    t = 0.0
+    per_P = {}
+    for Pw in Ps:
+        if y_gpu is None:  # the sweep: run each P again to have its output
+            yP, _ = sata.prefill(*pre, Pw, CHUNK, want_state=False)
+            torch.cuda.synchronize()
+        else:
+            yP = y_gpu
+        yh = yP.float().cpu().numpy()
+        errs, lds = [], []
+        for (b, h) in heads:
+            q, k, v = syn.make_head(wid, b, h, n, d, d, dt)
+            t0 = time.perf_counter()
+            yr, _, kap = oracle.taylor_attention_rows(q, k, v, Pw, rows)
+            t += time.perf_counter() - t0
+            errs.append(oracle.max_row_rel_error(yh[b, h, rows], yr, kap)[0])
+            if len(Ps) > 1:
+                lds.append(oracle.log10_abs_diff(yr, oracle.softmax_attention_rows(q, k, v, rows)))
+        entry = {"parity_max_row_rel_err": max(errs)}
+        if lds:
+            a = np.concatenate([x.ravel() for x in lds])
+            a = a[np.isfinite(a)]
+            entry["log10_abs_diff_vs_softmax"] = {"median": float(np.median(a)), "p99": float(np.percentile(a, 99)),
+                                                  "max": float(a.max())}
+        per_P[str(Pw)] = entry
+    out["value"] = len(heads) * len(rows) * len(Ps) / t / Hw
+    out["seconds"] = t
+    out["per_P"] = per_P
+    return out
 
 
 def main():
@@ -165,6 +325,9 @@ def main():
     import paper_2602_00294_amd as sata
     sata.load_library()
     assert torch.cuda.is_available(), "no GPU"
+    if args.workload != "headline":
+        print(json.dumps(run_workload(args, sata, torch)), flush=True)
+        return
 
     pre, dec = make_inputs(args.decode_steps)
     if args.copy_probe_mib > 0:
@@ -225,21 +388,6 @@ def main():
                 "work_per_launch": dec_bytes}
     dominant = roof_pre if pre_ms >= dec_ms else roof_dec
 
-    # parity spot check of what was just timed: first and last head, a few rows
-    import numpy as np
-
-    import oracle
-    import sata_synth as syn
-    torch.cuda.synchronize()
-    parity = {}
-    yh = y.float().cpu().numpy()
-    for (b, h) in ((0, 0), (B - 1, H - 1)):
-        q, k, v = syn.make_head(WORKLOAD_ID, b, h, N, DK, DV, "bf16")
-        rows = [0, 63, 64, 4095, N - 1]
-        yr, _, kap = oracle.taylor_attention_rows(q, k, v, P, rows)
-        err, _ = oracle.max_row_rel_error(yh[b, h, rows], yr, kap)
-        parity[f"b{b}h{h}"] = err
-
     line = {
         "metric": "prefill tokens/s + decode tokens/s (d_k=32,P=4); % MFMA/HBM roofline",
         "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -252,10 +400,10 @@ def main():
         "prefill_tokens_per_s": pre_tok_s, "decode_tokens_per_s": dec_tok_s,
         "prefill_ms": pre_ms, "decode_ms_per_step": dec_ms / args.decode_steps,
         "roofline": dominant, "rooflines": {"prefill": roof_pre, "decode": roof_dec},
-        "parity_max_row_rel_err": parity,
     }
     if not args.no_cpu_baseline:
-        cb = cpu_baseline(args.cpu_sample_heads, args.cpu_sample_decode_rows)
+        torch.cuda.synchronize()
+        cb = cpu_baseline(args.cpu_sample_heads, args.cpu_sample_decode_rows, y.float().cpu().numpy())
         whole = tokens / (B * N / cb["prefill_tokens_per_s"] + B * args.decode_steps / cb["decode_tokens_per_s"])
         cb["value"] = whole
         line["cpu_baseline"] = cb

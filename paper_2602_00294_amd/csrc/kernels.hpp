@@ -27,6 +27,7 @@ struct DecodePlan {
   int flat_tu = 0;  // > 0: whole-head float4 streaming kernel with this many threads in use
   size_t flat_lds = 0;
   int flat_msplit = 0;  // > 0: two workgroups per head, split after this many steps per thread
+  int flat_nth = 1024;  // threads per workgroup of the flat kernel (256 or 1024)
 };
 DecodePlan plan_decode(int64_t D, int dk, int dv);
 // partial: BH * nslices * (dv + 1) floats when nslices > 1, BH * 2 * (dv + 1)

@@ -614,17 +614,21 @@ DecodePlan plan_decode(int64_t D, int dk, int dv) {
     p.threads = D * E > 65536 ? 1024 : 256;
     // Such a head is streamed as flat float4s (decode_flat_kernel) when the
     // state is 16-byte aligned; the row-wise kernel stays for the others.
-    constexpr int nth = 1024;
+    // Heads of at most 256 KB of state take 256 threads (up to 8 heads stream
+    // on a CU at once), larger ones 1024.
+    const int nth = (D * E <= 65536 && 8 * E <= 256 && dk < 256) ? 256 : 1024;
     const int unit = E / std::gcd(E, 4);
     const int tu = (nth / unit) * unit;
     const size_t lds = sizeof(float2) * (size_t)D + sizeof(float) * (size_t)(2 * dk + E + 4 * tu + 9 * E + 16);
     if (tu > 0 && 8 * E <= nth && dk < nth && lds <= 150 * 1024) {
       p.flat_tu = tu;
       p.flat_lds = lds;
+      p.flat_nth = nth;
       // two pieces per head, the even-XCD one taking kFlatEvenShare of the
       // steps; two such workgroups fit a CU (LDS, and 64 VGPRs each)
       const int64_t steps = (D * E / 4 + tu - 1) / tu;
-      if (2 * lds <= 160 * 1024 && steps >= 4) p.flat_msplit = (int)(kFlatEvenShare * (double)steps + 0.5);
+      if (nth == 1024 && 2 * lds <= 160 * 1024 && steps >= 4)
+        p.flat_msplit = (int)(kFlatEvenShare * (double)steps + 0.5);
     }
     return p;
   }
@@ -648,14 +652,18 @@ hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, 
     // x d^(-1/4) for the closed-form P = 4 features (the float operations the
     // features would otherwise do per use); the table path scales by itself
     const float xscale = (t.P == 4) ? 1.0f / std::sqrt(std::sqrt((float)dk)) : 1.0f;
-#define SATA_DECODE_FLAT(TT)                                                                              \
-  e = hipFuncSetAttribute((const void*)decode_flat_kernel<TT, 1024>,                                      \
+#define SATA_DECODE_FLAT(TT, NTH)                                                                         \
+  e = hipFuncSetAttribute((const void*)decode_flat_kernel<TT, NTH>,                                       \
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)plan.flat_lds);                \
   if (e != hipSuccess) return e;                                                                          \
-  hipLaunchKernelGGL((decode_flat_kernel<TT, 1024>), dim3((unsigned)BH * (split ? 2u : 1u)), dim3(1024),        \
+  hipLaunchKernelGGL((decode_flat_kernel<TT, NTH>), dim3((unsigned)BH * (split ? 2u : 1u)), dim3(NTH),          \
                      plan.flat_lds, s, S, (const TT*)q, (const TT*)k, (const TT*)v, (TT*)y, t.packed, t.weight,   \
                      t.D, dk, dv, plan.flat_tu, t.P, xscale, plan.flat_msplit, split ? partial : nullptr, counters)
-    if (bf16) { SATA_DECODE_FLAT(bf16_t); } else { SATA_DECODE_FLAT(float); }
+    if (plan.flat_nth == 256) {
+      if (bf16) { SATA_DECODE_FLAT(bf16_t, 256); } else { SATA_DECODE_FLAT(float, 256); }
+    } else {
+      if (bf16) { SATA_DECODE_FLAT(bf16_t, 1024); } else { SATA_DECODE_FLAT(float, 1024); }
+    }
 #undef SATA_DECODE_FLAT
     return hipGetLastError();
   }
