@@ -26,13 +26,15 @@ struct DecodePlan {
   int threads = 0;  // workgroup size
   int flat_tu = 0;  // > 0: whole-head float4 streaming kernel with this many threads in use
   size_t flat_lds = 0;
-  int flat_msplit = 0;  // > 0: two workgroups per head, split after this many steps per thread
   int flat_nth = 1024;  // threads per workgroup of the flat kernel (256 or 1024)
+  int flat_np = 1;      // workgroups (pieces) per head
+  int flat_steps = 0;   // float4 steps per thread over a whole head
+  int flat_rows = 0;    // state rows a piece touches at most (its feature values in LDS)
 };
-DecodePlan plan_decode(int64_t D, int dk, int dv);
-// partial: BH * nslices * (dv + 1) floats when nslices > 1, BH * 2 * (dv + 1)
-// when flat_msplit > 0; counters: BH ints, all zero, when flat_msplit > 0 (the
-// kernel leaves them zero).  Without them a split plan runs unsplit.
+DecodePlan plan_decode(int64_t D, int dk, int dv, int BH);
+// partial: BH * n * (dv + 1) floats with n = nslices when nslices > 1 and the
+// state is not 16-byte aligned, n = flat_np when flat_np > 1; counters: BH
+// ints, all zero, when flat_np > 1 (the kernel leaves them zero).
 hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, void* y, bool bf16,
                          int BH, int dk, int dv, const DevTable& t, const DecodePlan& plan,
                          float* partial, int* counters, hipStream_t s);

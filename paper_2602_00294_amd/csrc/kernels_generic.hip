@@ -146,14 +146,16 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(
 // order at the end, so the result is deterministic.  Loads run two groups of
 // kFlatUnroll float4s ahead of the arithmetic.
 //
-// With xpart given, each head is streamed by two workgroups (blockIdx =
-// 2 head + piece): piece 0 takes a thread's steps m < msplit, piece 1 the
-// rest.  The hardware deals workgroups to the 8 XCDs in turn, so piece 0 runs
-// on the even-numbered XCDs and piece 1 on the odd ones, which stream this
-// pattern about a quarter more slowly; msplit sizes the pieces to match.
-// Each piece stores its E column sums at xpart[2 head + piece] with device-
-// coherent stores and bumps cnt[head]; the second to arrive adds the two (a
-// sum of two terms, so the result does not depend on which one it is), writes
+// With npieces > 1 (an even number), each head is streamed by that many
+// workgroups (blockIdx = npieces head + piece), piece p taking a thread's
+// steps [m(p), m(p+1)).  The hardware deals workgroups to the 8 XCDs in turn,
+// so even pieces run on even-numbered XCDs and odd pieces on odd ones, which
+// stream this pattern about a quarter more slowly: of each (even, odd) pair
+// the even piece takes the share kFlatEvenShare of the steps.  Each piece
+// needs the features of its own rows only, kept in LDS from its first row on.
+// Each piece stores its E column sums at xpart[npieces head + piece] with
+// device-coherent stores and bumps cnt[head]; the last to arrive adds them in
+// piece order (so the result does not depend on the order of arrival), writes
 // y and sets the counter back to 0.  No device-scope fence is used: one would
 // write back the XCD's whole L2, full of freshly written state.
 constexpr int kFlatUnroll = 2;
@@ -165,20 +167,26 @@ template <typename T, int NTH>
 __global__ void __launch_bounds__(NTH, 8)
 decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __restrict__ k,
                    const T* __restrict__ v, T* __restrict__ y, const uint64_t* __restrict__ packed,
-                   const float* __restrict__ weight, int64_t D, int dk, int dv, int tu, int P, float xscale,
-                   int msplit, float* __restrict__ xpart, int* __restrict__ cnt) {
+                   const float* __restrict__ weight, int64_t D, int dk, int dv, int tu, int P, int closed,
+                   float xscale, int npieces, int steps, int max_rows, float* __restrict__ xpart,
+                   int* __restrict__ cnt) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
   const int E = dv + 1;
   const int tid = threadIdx.x;
-  const bool split = xpart != nullptr;
-  const int piece = split ? (int)(blockIdx.x & 1) : 0;
-  const int64_t bh = split ? (int64_t)(blockIdx.x >> 1) : (int64_t)blockIdx.x;
-  const int64_t m_lo = piece ? msplit : 0;
-  const int64_t m_hi = (split && piece == 0) ? msplit : ((int64_t)1 << 40);
+  const bool split = npieces > 1;
+  const int piece = (int)(blockIdx.x % (unsigned)npieces);
+  const int64_t bh = (int64_t)(blockIdx.x / (unsigned)npieces);
+  // the piece's steps: the first piece starts at 0 and the last runs to the end
+  auto step_of = [&](int p) -> int64_t {
+    const float w = (float)(p >> 1) + ((p & 1) ? (float)kFlatEvenShare : 0.0f);
+    return (int64_t)(w * 2.0f / (float)npieces * (float)steps + 0.5f);
+  };
+  const int64_t m_lo = (piece == 0) ? 0 : step_of(piece);
+  const int64_t m_hi = (piece == npieces - 1) ? ((int64_t)1 << 40) : step_of(piece + 1);
   const int64_t N = D * E;
   float* const Sh = S + bh * N;
-  float2* const fkq = (float2*)lds;        // [D] {phi_k, phi_q}
-  float* const xq = (float*)(fkq + D);     // [dk]
+  float2* const fkq = (float2*)lds;        // [max_rows] {phi_k, phi_q} of rows row_lo..
+  float* const xq = (float*)(fkq + max_rows);  // [dk]
   float* const xk = xq + dk;               // [dk]
   float* const ve = xk + dk;               // [E]
   float* const red = ve + E;               // [4 tu] per-thread column sums
@@ -192,17 +200,16 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
   const float4* const Sv = (const float4*)(Sh + a0);
   const bool active = tid < tu;
   // leftover elements [0, a0) and [a0 + 4 nv, N): one per thread of the last
-  // wave; a split head's first piece takes the leading ones, its second the
-  // trailing ones
-  const int nlead = (split && piece == 1) ? 0 : (int)min<int64_t>(a0, N);
-  const int ntrail = (split && piece == 0) ? 0 : (int)(N - (a0 + 4 * nv));
+  // wave; the first piece takes the leading ones, the last the trailing ones
+  const int nlead = (piece == 0) ? (int)min<int64_t>(a0, N) : 0;
+  const int ntrail = (piece == npieces - 1) ? (int)(N - (a0 + 4 * nv)) : 0;
   const int nleft = nlead + ntrail;
   const int lt = tid - (NTH - 8);
   const int64_t le = (lt < nlead) ? lt : a0 + 4 * nv + (lt - nlead);
-  // the state rows this workgroup touches (a split piece needs only its own)
-  const int64_t e_split = a0 + 4 * min<int64_t>(nv, (int64_t)tu * msplit);
-  const int64_t row_lo = (split && piece == 1) ? min<int64_t>(D - 1, e_split / E) : 0;
-  const int64_t row_hi = (split && piece == 0) ? (e_split - 1) / E : D - 1;
+  // the state rows this workgroup touches: its features are kept from row_lo on
+  const int64_t row_lo = (piece == 0) ? 0 : min<int64_t>(D - 1, (a0 + 4 * min<int64_t>(nv, (int64_t)tu * m_lo)) / E);
+  const int64_t row_hi =
+      (piece == npieces - 1) ? D - 1 : max<int64_t>(row_lo, (a0 + 4 * min<int64_t>(nv, (int64_t)tu * m_hi) - 1) / E);
   // q, k, v go to LDS first (in the first wave, which waits for them there),
   // then every wave sends its first state loads, which stay in flight while
   // the features are computed: the barriers below wait for LDS only
@@ -222,7 +229,7 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
   }
   lx = lead ? lx : 0.0f;
   lds_barrier();
-  if (P == 4) {
+  if (closed) {
     // Features in closed form, no table (LDS holds x~ = x d^(-1/4)).  Work
     // items are (prefix i1 <= i2, block h of up to 8 third indices i3 in
     // [i2 + 8h, i2 + 8h + 8)); tier h holds the prefixes with i2 < d - 8h,
@@ -234,6 +241,7 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
     // workgroup's rows are skipped.
     const int npair = dk * (dk + 1) / 2;
     const int base2 = 1 + dk, base3 = 1 + dk + npair;
+    const int rlo32 = (int)row_lo, rhi32 = (int)row_hi;  // (a closed-form head has D < 2^31 rows)
     int nitems = 0;
     for (int m = dk; m > 0; m -= 8) nitems += m * (m + 1) / 2;
     for (int it = tid; it < nitems; it += NTH) {
@@ -251,15 +259,19 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
       if (h == 0) {
         const int row2 = base2 + i1 * dk - i1 * (i1 - 1) / 2 + (i2 - i1);
         const float w2 = (i1 == i2) ? 0.70710678118654752f : 1.0f;
-        if (row2 >= row_lo && row2 <= row_hi) fkq[row2] = float2{ka * kb * w2, qa * qb * w2};
+        if (row2 >= rlo32 && row2 <= rhi32) fkq[row2 - rlo32] = float2{ka * kb * w2, qa * qb * w2};
       }
       // degree-3 tuples before (i1, i2, i2): all with a smaller first index,
       // then first index i1 and second index in [i1, i2)
       const int start3 = base3 + (dk + 2) * (dk + 1) * dk / 6 - (dk - i1 + 2) * (dk - i1 + 1) * (dk - i1) / 6 +
                          (i2 - i1) * dk - (i2 * (i2 - 1) - i1 * (i1 - 1)) / 2;
       const int j0 = i2 + 8 * h;
-      const int64_t rfirst = start3 + (j0 - i2);
-      if (rfirst > row_hi || rfirst + 7 < row_lo) continue;
+      // the item's features u = 0..7 (rows rfirst + u) that exist (i3 < d) and
+      // fall in this workgroup's rows
+      const int rfirst = start3 + (j0 - i2);
+      const int ulo = max(0, rlo32 - rfirst);
+      const int uhi = min(min(8, dk - j0), rhi32 - rfirst + 1);
+      if (ulo >= uhi) continue;
       const float pq = qa * qb, pk = ka * kb;
       // 1 / sqrt(prod c!): three equal indices (1/sqrt(6)) only at i3 = i2 = i1,
       // two (1/sqrt(2)) at i3 = i2 or i1 = i2
@@ -271,29 +283,27 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
         const int ic = min(i3, dk - 1);  // in range, so the reads need no guard
         const float xk3 = xk[ic], xq3 = xq[ic];
         const float w3 = (u == 0) ? wfirst : wrest;
-        if (i3 < dk) fkq[start3 + (i3 - i2)] = float2{pk * xk3 * w3, pq * xq3 * w3};
+        if ((unsigned)(u - ulo) < (unsigned)(uhi - ulo)) fkq[rfirst - rlo32 + u] = float2{pk * xk3 * w3, pq * xq3 * w3};
       }
     }
     const int t1 = NTH - 1 - tid;
-    if (t1 == 0)
-      fkq[0] = float2{1.0f, 1.0f};
-    else if (t1 <= dk)
-      fkq[t1] = float2{xk[t1 - 1], xq[t1 - 1]};
+    if (t1 <= dk && t1 >= rlo32 && t1 <= rhi32)
+      fkq[t1 - rlo32] = (t1 == 0) ? float2{1.0f, 1.0f} : float2{xk[t1 - 1], xq[t1 - 1]};
   } else {
-    // the table entries of up to 8 features per thread are loaded together
-    for (int64_t fb = tid; fb < D; fb += 8 * NTH) {
+    // the table entries of up to 8 of the rows per thread are loaded together
+    for (int64_t fb = row_lo + tid; fb <= row_hi; fb += 8 * NTH) {
       uint64_t pk[8];
       float w[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int64_t f = fb + (int64_t)NTH * u;
-        pk[u] = (f < D) ? packed[f] : 0;
-        w[u] = (f < D) ? weight[f] : 0.0f;
+        pk[u] = (f <= row_hi) ? packed[f] : 0;
+        w[u] = (f <= row_hi) ? weight[f] : 0.0f;
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int64_t f = fb + (int64_t)NTH * u;
-        if (f < D) fkq[f] = float2{feature_value(pk[u], w[u], xk), feature_value(pk[u], w[u], xq)};
+        if (f <= row_hi) fkq[f - row_lo] = float2{feature_value(pk[u], w[u], xk), feature_value(pk[u], w[u], xq)};
       }
     }
   }
@@ -301,7 +311,7 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
   if (lt >= 0 && lt < nleft) {
     const int64_t f = le / E;
     const int j = (int)(le - f * E);
-    const float2 fw = fkq[f];
+    const float2 fw = fkq[f - row_lo];
     lx += fw.x * ve[j];
     Sh[le] = lx;
     lo_val[lt] = fw.y * lx;
@@ -318,6 +328,7 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
     f0[c] = e / E;
     vj[c] = ve[e - f0[c] * E];
     acc[c] = 0.0f;
+    f0[c] -= (int)row_lo;  // positions in the piece's feature rows
   }
   float4* const Sw = (float4*)(Sh + a0);
   if (active) {
@@ -374,15 +385,34 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
   __syncthreads();
   if (split) {
     if (tid < E)
-      __hip_atomic_store(xpart + (bh * 2 + piece) * E + tid, o[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(xpart + (bh * npieces + piece) * E + tid, o[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __builtin_amdgcn_s_waitcnt(0);  // the stores have completed before the count goes up
     __syncthreads();
     int* const arrived = (int*)red;  // (the column sums are no longer needed)
     if (tid == 0) arrived[0] = __hip_atomic_fetch_add(cnt + bh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
-    if (arrived[0] == 0) return;  // the other piece finishes the head
-    if (tid < E)
-      o[tid] += __hip_atomic_load(xpart + (bh * 2 + (piece ^ 1)) * E + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (arrived[0] != npieces - 1) return;  // a later piece finishes the head
+    if (npieces == 2) {  // (a two-term sum does not depend on the order)
+      if (tid < E)
+        o[tid] += __hip_atomic_load(xpart + (bh * 2 + (piece ^ 1)) * E + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else if (tid < E) {
+      // the other pieces' sums, 8 loads in flight at a time, added in piece order
+      // (this piece's own from LDS)
+      const float* const xp = xpart + bh * npieces * E + tid;
+      float a = 0.0f;
+      for (int p0 = 0; p0 < npieces; p0 += 8) {
+        float w[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          w[u] = (p0 + u < npieces && p0 + u != piece)
+                     ? __hip_atomic_load(xp + (p0 + u) * E, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                     : 0.0f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (p0 + u < npieces) a += (p0 + u == piece) ? o[tid] : w[u];
+      }
+      o[tid] = a;
+    }
     if (tid == 0) __hip_atomic_store(cnt + bh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
   }
@@ -603,42 +633,55 @@ hipError_t launch_feature_map(const void* x, bool bf16, int64_t rows, const DevT
   return hipSuccess;
 }
 
-DecodePlan plan_decode(int64_t D, int dk, int dv) {
+DecodePlan plan_decode(int64_t D, int dk, int dv, int BH) {
   const int E = dv + 1;
   DecodePlan p;
-  // A head whose feature values fit in LDS next to nothing else is streamed by
-  // one workgroup (no cross-workgroup reduction, one launch per step).
+  // Row-wise plans, used when the state is not 16-byte aligned: a head whose
+  // feature values fit in LDS is streamed by one workgroup, a larger one in
+  // feature slices of about 32K state elements (128 KB of float32) with a
+  // second launch adding the slices' sums.
   if (2 * D * (int64_t)sizeof(float) <= 96 * 1024) {
     p.fps = (int)D;
     p.nslices = 1;
     p.threads = D * E > 65536 ? 1024 : 256;
-    // Such a head is streamed as flat float4s (decode_flat_kernel) when the
-    // state is 16-byte aligned; the row-wise kernel stays for the others.
-    // Heads of at most 256 KB of state take 256 threads (up to 8 heads stream
-    // on a CU at once), larger ones 1024.
-    const int nth = (D * E <= 65536 && 8 * E <= 256 && dk < 256) ? 256 : 1024;
-    const int unit = E / std::gcd(E, 4);
-    const int tu = (nth / unit) * unit;
-    const size_t lds = sizeof(float2) * (size_t)D + sizeof(float) * (size_t)(2 * dk + E + 4 * tu + 9 * E + 16);
-    if (tu > 0 && 8 * E <= nth && dk < nth && lds <= 150 * 1024) {
-      p.flat_tu = tu;
-      p.flat_lds = lds;
-      p.flat_nth = nth;
-      // two pieces per head, the even-XCD one taking kFlatEvenShare of the
-      // steps; two such workgroups fit a CU (LDS, and 64 VGPRs each)
-      const int64_t steps = (D * E / 4 + tu - 1) / tu;
-      if (nth == 1024 && 2 * lds <= 160 * 1024 && steps >= 4)
-        p.flat_msplit = (int)(kFlatEvenShare * (double)steps + 0.5);
-    }
-    return p;
+  } else {
+    int64_t fps = std::max<int64_t>(kThreads / E, (32768 + E - 1) / E);
+    fps = std::min<int64_t>(fps, 4096);
+    fps = std::min<int64_t>(fps, D);
+    p.fps = (int)fps;
+    p.nslices = (int)((D + fps - 1) / fps);
+    p.threads = kThreads;
   }
-  // Larger heads: about 32K state elements (128 KB of float32) per workgroup.
-  int64_t fps = std::max<int64_t>(kThreads / E, (32768 + E - 1) / E);
-  fps = std::min<int64_t>(fps, 4096);
-  fps = std::min<int64_t>(fps, D);
-  p.fps = (int)fps;
-  p.nslices = (int)((D + fps - 1) / fps);
-  p.threads = kThreads;
+  // The flat float4 stream (decode_flat_kernel).  Heads of at most 256 KB of
+  // state take one 256-thread workgroup each (up to 8 stream on a CU at once);
+  // larger heads 1024-thread workgroups, an even number of pieces per head:
+  // two, or more while the grid has fewer than 512 workgroups and every piece
+  // keeps at least 8 steps per thread.
+  const int nth = (D * E <= 65536 && 8 * E <= 256 && dk < 256) ? 256 : 1024;
+  const int unit = E / std::gcd(E, 4);
+  const int tu = (nth / unit) * unit;
+  if (tu <= 0 || 8 * E > nth || dk >= nth) return p;
+  const int64_t steps = (D * E / 4 + tu - 1) / tu;
+  int np = 1;
+  if (nth == 1024 && steps >= 4) {
+    np = 2;
+    while ((int64_t)BH * np < 512 && steps / (2 * np) >= 8 && np < 64) np *= 2;
+  }
+  // rows a piece touches at most: its steps (the larger share of a pair, plus
+  // rounding) times 4 tu elements, and the rows cut at both ends
+  int64_t rows = D;
+  if (np > 1) {
+    const int64_t piece_steps = (int64_t)(kFlatEvenShare * 2.0 / np * (double)steps) + 2;
+    rows = std::min<int64_t>(D, (4 * tu * piece_steps + 3) / E + 3);
+  }
+  const size_t lds = sizeof(float2) * (size_t)rows + sizeof(float) * (size_t)(2 * dk + E + 4 * tu + 9 * E + 16);
+  if (lds > 150 * 1024) return p;
+  p.flat_tu = tu;
+  p.flat_lds = lds;
+  p.flat_nth = nth;
+  p.flat_np = np;
+  p.flat_steps = (int)steps;
+  p.flat_rows = (int)rows;
   return p;
 }
 
@@ -648,17 +691,22 @@ hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, 
   const int E = dv + 1;
   if (plan.flat_tu > 0 && ((uintptr_t)S & 15) == 0) {
     hipError_t e;
-    const bool split = plan.flat_msplit > 0 && partial != nullptr && counters != nullptr;
-    // x d^(-1/4) for the closed-form P = 4 features (the float operations the
-    // features would otherwise do per use); the table path scales by itself
-    const float xscale = (t.P == 4) ? 1.0f / std::sqrt(std::sqrt((float)dk)) : 1.0f;
+    if (plan.flat_np > 1 && (partial == nullptr || counters == nullptr)) return hipErrorInvalidValue;
+    // Closed-form features for P = 4 when a piece's rows are a large part of
+    // the head; the feature table otherwise.  The closed form takes the
+    // coordinates already scaled by d^(-1/4) (computed here with the float
+    // operations the features would otherwise do per use); the table path
+    // scales by itself.
+    const int closed = (t.P == 4 && plan.flat_np <= 2) ? 1 : 0;
+    const float xscale = closed ? 1.0f / std::sqrt(std::sqrt((float)dk)) : 1.0f;
 #define SATA_DECODE_FLAT(TT, NTH)                                                                         \
   e = hipFuncSetAttribute((const void*)decode_flat_kernel<TT, NTH>,                                       \
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)plan.flat_lds);                \
   if (e != hipSuccess) return e;                                                                          \
-  hipLaunchKernelGGL((decode_flat_kernel<TT, NTH>), dim3((unsigned)BH * (split ? 2u : 1u)), dim3(NTH),          \
+  hipLaunchKernelGGL((decode_flat_kernel<TT, NTH>), dim3((unsigned)BH * (unsigned)plan.flat_np), dim3(NTH),       \
                      plan.flat_lds, s, S, (const TT*)q, (const TT*)k, (const TT*)v, (TT*)y, t.packed, t.weight,   \
-                     t.D, dk, dv, plan.flat_tu, t.P, xscale, plan.flat_msplit, split ? partial : nullptr, counters)
+                     t.D, dk, dv, plan.flat_tu, t.P, closed, xscale, plan.flat_np, plan.flat_steps, plan.flat_rows, \
+                     partial, counters)
     if (plan.flat_nth == 256) {
       if (bf16) { SATA_DECODE_FLAT(bf16_t, 256); } else { SATA_DECODE_FLAT(float, 256); }
     } else {

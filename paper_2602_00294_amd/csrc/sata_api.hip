@@ -303,18 +303,18 @@ sata_status sata_decode_step(float* S, const void* q, const void* k, const void*
   hipStream_t s = (hipStream_t)stream;
   sata::DevTable t;
   if ((st = get_table(d_k, P, s, &t)) != SATA_OK) return st;
-  sata::DecodePlan plan = sata::plan_decode(D, d_k, d_v);
+  sata::DecodePlan plan = sata::plan_decode(D, d_k, d_v, BH);
   float* partial = nullptr;
   int* counters = nullptr;
-  // partial sums: one row per slice, or per piece of a head split in two
-  const int64_t rows = (plan.nslices > 1) ? plan.nslices : (plan.flat_msplit > 0 ? 2 : 0);
+  // partial sums: one row per slice (row-wise path) or per piece of a head (flat path)
+  const int64_t rows = std::max<int64_t>(plan.nslices > 1 ? plan.nslices : 0, plan.flat_np > 1 ? plan.flat_np : 0);
   if (rows > 0) {
     void* ws = nullptr;
     const size_t bytes = sizeof(float) * (size_t)BH * rows * (d_v + 1);
     if ((st = get_workspace(bytes, s, &ws)) != SATA_OK) return st;
     partial = (float*)ws;
   }
-  if (plan.flat_msplit > 0 && (st = get_counters(BH, s, &counters)) != SATA_OK) return st;
+  if (plan.flat_np > 1 && (st = get_counters(BH, s, &counters)) != SATA_OK) return st;
   hipError_t e =
       sata::launch_decode(S, q, k, v, y, dt == SATA_BF16, BH, d_k, d_v, t, plan, partial, counters, s);
   if (e != hipSuccess) return hip_fail(e, "decode launch");
