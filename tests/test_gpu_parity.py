@@ -218,3 +218,48 @@ def test_decode_unaligned_state(sata):
         yr, Sr = oracle.decode_ref(S0[0, h], q[0, h, :1], k[0, h, :1], v[0, h, :1], P)
         assert max_row_rel_error(y[0, h][None], yr)[0] < 1e-4
         assert state_rel_error(to_host(S)[0, h], Sr) < 1e-6
+
+
+def test_decode_unaligned_large_state(sata):
+    """A large head (d=64, feature values beyond LDS) whose state is not
+    16-byte aligned takes the row-wise kernel in feature slices plus the
+    launch that adds their sums."""
+    rng = np.random.default_rng(13)
+    B, H, d, P = 1, 2, 64, 4
+    D = oracle.feature_count(d, P)
+    S0 = _random_state(rng, B, H, D, d)
+    flat = torch.zeros(S0.size + 1, device="cuda")
+    S = flat[1:].view(S0.shape)                    # offset by one float
+    S.copy_(torch.from_numpy(S0).cuda())
+    assert S.data_ptr() % 16 != 0
+    q, k, v = syn.make_qkv(61, B, H, 1, d, d, "f32")
+    y = to_host(sata.decode_step(S, to_dev(q[:, :, 0].copy(), "f32"), to_dev(k[:, :, 0].copy(), "f32"),
+                                 to_dev(v[:, :, 0].copy(), "f32"), P))
+    torch.cuda.synchronize()
+    Sh = to_host(S)
+    for h in range(H):
+        yr, Sr = oracle.decode_ref(S0[0, h], q[0, h, :1], k[0, h, :1], v[0, h, :1], P)
+        assert max_row_rel_error(y[0, h][None], yr)[0] < 1e-4
+        assert state_rel_error(Sh[0, h], Sr) < 1e-6
+
+
+def test_decode_many_pieces_per_head(sata):
+    """Few large heads: each is streamed by several pieces (d=64: D=47905,
+    12.5 MB of state per head), bf16 inputs, two steps in a row."""
+    rng = np.random.default_rng(14)
+    B, H, d, P = 1, 3, 64, 4
+    D = oracle.feature_count(d, P)
+    S0 = _random_state(rng, B, H, D, d)
+    S = torch.from_numpy(S0).cuda()
+    q, k, v = syn.make_qkv(62, B, H, 2, d, d, "bf16")
+    ys = []
+    for t in range(2):
+        ys.append(to_host(sata.decode_step(S, to_dev(q[:, :, t].copy(), "bf16"), to_dev(k[:, :, t].copy(), "bf16"),
+                                           to_dev(v[:, :, t].copy(), "bf16"), P)))
+    torch.cuda.synchronize()
+    Sh = to_host(S)
+    for h in range(H):
+        yr, Sr = oracle.decode_ref(S0[0, h], q[0, h, :2], k[0, h, :2], v[0, h, :2], P)
+        got = np.stack([yy[0, h] for yy in ys])
+        assert max_row_rel_error(got, yr)[0] < TOL["bf16"]
+        assert state_rel_error(Sh[0, h], Sr) < 1e-6
