@@ -478,13 +478,16 @@ prefill_generic_main(const T* __restrict__ q, const T* __restrict__ k, const T* 
                      const uint64_t* __restrict__ packed, const float* __restrict__ weight, int64_t D,
                      float* __restrict__ S_state, float* __restrict__ part, int BH, int n, int dk, int dv,
                      int C, int FS, int seg0, int seg_len, int first_seg) {
-  extern __shared__ float lds[];
+  // FS: features per slice, a multiple of 4 (the last slice may hold fewer, fs)
+  extern __shared__ __attribute__((aligned(16))) float lds[];
   const int E = dv + 1;
-  float* Sl = lds;              // [FS][E]
-  float* fb = Sl + FS * E;      // [C][FS]
+  float* Sl = lds;              // [FS][E] this slice of the state
+  float* fb = Sl + FS * E;      // [C][FS] feature values of the chunk (q, then k)
   float* xq = fb + C * FS;      // [C][dk]
   float* xk = xq + C * dk;      // [C][dk]
   float* ve = xk + C * dk;      // [C][E]
+  uint64_t* tpk = (uint64_t*)(ve + C * E);  // [FS] the slice's table entries
+  float* tw = (float*)(tpk + FS);           // [FS]
   const int s = blockIdx.x;
   const int64_t bh = blockIdx.y;
   const int tid = threadIdx.x;
@@ -493,6 +496,11 @@ prefill_generic_main(const T* __restrict__ q, const T* __restrict__ k, const T* 
   float* Sg = S_state + (bh * D + f0) * E;
 
   for (int i = tid; i < fs * E; i += kThreads) Sl[i] = first_seg ? 0.0f : Sg[i];
+  for (int f = tid; f < fs; f += kThreads) {
+    tpk[f] = packed[f0 + f];
+    tw[f] = weight[f0 + f];
+  }
+  const int TQ = C / 4;  // readout tiles: tokens tq + TQ u, u = 0..3
 
   const int seg_end = min(n, seg0 + seg_len);
   for (int t0 = seg0; t0 < seg_end; t0 += C) {
@@ -503,33 +511,61 @@ prefill_generic_main(const T* __restrict__ q, const T* __restrict__ k, const T* 
     for (int i = tid; i < cn * fs; i += kThreads) {
       const int t = i / fs;
       const int f = i - t * fs;
-      fb[t * FS + f] = feature_value(packed[f0 + f], weight[f0 + f], xq + t * dk);
+      fb[t * FS + f] = feature_value(tpk[f], tw[f], xq + t * dk);
     }
     __syncthreads();
-    // inter-chunk readout against the state before this chunk
+    // inter-chunk readout against the state before this chunk: each thread
+    // sums 4 tokens x 1 value column, 4 features per step
     float* pout = part + (((int64_t)s * BH + bh) * seg_len + (t0 - seg0)) * E;
-    for (int o = tid; o < cn * E; o += kThreads) {
-      const int t = o / E;
-      const int j = o - t * E;
-      const float* a = fb + t * FS;
-      float acc = 0.0f;
-      for (int f = 0; f < fs; ++f) acc += a[f] * Sl[f * E + j];
-      pout[o] = acc;
+    for (int tile = tid; tile < TQ * E; tile += kThreads) {
+      const int tq = tile / E;
+      const int j = tile - tq * E;
+      float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      int f = 0;
+      for (; f + 4 <= fs; f += 4) {
+        const float s0 = Sl[f * E + j], s1 = Sl[(f + 1) * E + j], s2 = Sl[(f + 2) * E + j], s3 = Sl[(f + 3) * E + j];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float4 a = *(const float4*)(fb + (tq + TQ * u) * FS + f);
+          acc[u] += a.x * s0 + a.y * s1 + a.z * s2 + a.w * s3;
+        }
+      }
+      for (; f < fs; ++f) {
+        const float s0 = Sl[f * E + j];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc[u] += fb[(tq + TQ * u) * FS + f] * s0;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (tq + TQ * u < cn) pout[(tq + TQ * u) * E + j] = acc[u];
     }
     __syncthreads();
     for (int i = tid; i < cn * fs; i += kThreads) {
       const int t = i / fs;
       const int f = i - t * fs;
-      fb[t * FS + f] = feature_value(packed[f0 + f], weight[f0 + f], xk + t * dk);
+      fb[t * FS + f] = feature_value(tpk[f], tw[f], xk + t * dk);
     }
     __syncthreads();
-    // state update with this chunk's keys and values
-    for (int o = tid; o < fs * E; o += kThreads) {
-      const int f = o / E;
-      const int j = o - f * E;
-      float acc = 0.0f;
-      for (int t = 0; t < cn; ++t) acc += fb[t * FS + f] * ve[t * E + j];
-      Sl[o] += acc;
+    // state update with this chunk's keys and values: each thread sums 4
+    // features x 1 value column over the chunk's tokens (columns of fb past
+    // fs feed only sums that are not stored)
+    for (int tile = tid; tile < (FS / 4) * E; tile += kThreads) {
+      const int fg = tile / E;
+      const int j = tile - fg * E;
+      const int f = 4 * fg;
+      if (f >= fs) continue;
+      float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      for (int t = 0; t < cn; ++t) {
+        const float4 a = *(const float4*)(fb + t * FS + f);
+        const float vv = ve[t * E + j];
+        acc[0] += a.x * vv;
+        acc[1] += a.y * vv;
+        acc[2] += a.z * vv;
+        acc[3] += a.w * vv;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (f + u < fs) Sl[(f + u) * E + j] += acc[u];
     }
   }
   __syncthreads();
@@ -763,17 +799,22 @@ bool plan_prefill_generic(int64_t D, int BH, int n, int dk, int dv, int chunk, s
   const int E = dv + 1;
   const int C = chunk;
   const size_t fixed = sizeof(float) * ((size_t)2 * C * dk + (size_t)C * E);
-  const size_t per_feature = sizeof(float) * ((size_t)E + C);
+  // per feature: its state row, its column of chunk feature values and its table entry
+  const size_t per_feature = sizeof(float) * ((size_t)E + C) + sizeof(uint64_t) + sizeof(float);
   if (fixed + 8 * per_feature > kLdsBudget) return false;
   int64_t fs = (int64_t)((kLdsBudget - fixed) / per_feature);
   fs = std::min<int64_t>(fs, 512);
+  // enough slices for about 4 workgroups per CU, but at least 32 features each
+  const int64_t want = (1024 + BH - 1) / BH;
+  fs = std::min<int64_t>(fs, std::max<int64_t>(32, (D + want - 1) / want));
   fs = std::min<int64_t>(fs, D);
+  fs = std::max<int64_t>(4, fs / 4 * 4);  // a multiple of 4
   plan->fs = (int)fs;
   plan->nslices = (int)((D + fs - 1) / fs);
   plan->lds_main = fixed + per_feature * (size_t)fs;
   plan->lds_final = sizeof(float) * ((size_t)2 * C * dk + (size_t)C * E + (size_t)kFinRows * C +
                                      (size_t)kFinRows * E);
-  if (plan->lds_final > kLdsBudget) return false;
+  if (plan->lds_main > kLdsBudget || plan->lds_final > kLdsBudget) return false;
   // partial readouts for one segment: [nslices][BH][seg_len][E]
   const size_t per_token = sizeof(float) * (size_t)plan->nslices * BH * E;
   int64_t seg = (int64_t)(max_ws_bytes / per_token);
