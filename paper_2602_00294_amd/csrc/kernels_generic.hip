@@ -54,6 +54,8 @@ feature_map_kernel(const T* __restrict__ x, int64_t rows, int d, const uint64_t*
 // touch consecutive addresses, each element is updated (S += phi_k[f] * [v|1][j])
 // and immediately read out (o_j += phi_q[f] * S).  Large heads are split over
 // several workgroups instead (decode_slice_kernel + decode_finalize_kernel).
+// These row-wise kernels serve states that are not 16-byte aligned; aligned
+// ones take the flat float4 stream (decode_flat_kernel).
 template <typename T, int NTH>
 __device__ __forceinline__ void decode_rows(float* __restrict__ S, const T* __restrict__ q,
                                             const T* __restrict__ k, const T* __restrict__ v,
