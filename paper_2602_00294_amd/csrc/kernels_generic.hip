@@ -803,8 +803,15 @@ bool plan_prefill_generic(int64_t D, int BH, int n, int dk, int dv, int chunk, s
   const size_t fixed = sizeof(float) * ((size_t)2 * C * dk + (size_t)C * E);
   // per feature: its state row, its column of chunk feature values and its table entry
   const size_t per_feature = sizeof(float) * ((size_t)E + C) + sizeof(uint64_t) + sizeof(float);
-  if (fixed + 8 * per_feature > kLdsBudget) return false;
-  int64_t fs = (int64_t)((kLdsBudget - fixed) / per_feature);
+  // LDS per workgroup: every slice re-reads the chunk's q, k, v tiles, so
+  // slices are as wide as LDS allows when those tiles are large; when they are
+  // small, narrower slices let several workgroups share a CU (one per CU
+  // leaves the latency of one wave per SIMD exposed)
+  const size_t budget = (fixed <= ((size_t)16 << 10)) ? ((size_t)40 << 10)
+                        : (fixed <= ((size_t)32 << 10)) ? ((size_t)76 << 10)
+                                                         : kLdsBudget;
+  if (fixed + 8 * per_feature > budget) return false;
+  int64_t fs = (int64_t)((budget - fixed) / per_feature);
   fs = std::min<int64_t>(fs, 512);
   // enough slices for about 4 workgroups per CU, but at least 32 features each
   const int64_t want = (1024 + BH - 1) / BH;
