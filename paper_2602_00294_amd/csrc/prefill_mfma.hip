@@ -291,9 +291,12 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   // Slice-major workgroup order: the hardware deals workgroups to the 8 XCDs
   // in turn, so with heads innermost every XCD gets every slice kind (the
-  // kinds differ in cost) instead of a fixed one.
-  const int slice = (int)(blockIdx.x / (unsigned)BH);
-  const int64_t bh = blockIdx.x - (int64_t)slice * BH;
+  // kinds differ in cost) instead of a fixed one.  The division runs on the
+  // vector unit; reading its result back into scalar registers keeps the head
+  // offsets and every pointer derived from them scalar, instead of in spilled
+  // vector registers.
+  const int slice = __builtin_amdgcn_readfirstlane((int)(blockIdx.x / (unsigned)BH));
+  const int64_t bh = __builtin_amdgcn_readfirstlane((int)(blockIdx.x - (unsigned)slice * BH));
   const int4 sl = slices[slice];
   const int lo = __builtin_amdgcn_readfirstlane(sl.x);
   const int nc = __builtin_amdgcn_readfirstlane(sl.y);
