@@ -72,6 +72,10 @@ FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
     ((0, 1, 1, 8, 4, 4, 9, 64, FAKE), -1),       # P > 8
     ((0, 1, 1, 8, 4, 4, 4, 48, FAKE), -2),       # unsupported chunk
     ((0, 1, 1, 8, 200, 4, 8, 64, FAKE), -3),     # feature count too large
+    ((0, 1, 1, 8, 256, 4, 2, 64, FAKE), -1),     # d_k > 255
+    ((0, 1, 1, 8, 4, 256, 2, 64, FAKE), -1),     # d_v > 255
+    ((0, 2, 32768, 8, 4, 4, 4, 64, FAKE), -3),   # B*H = 65536 > 65535
+    ((1, 1, 65536, 8, 4, 4, 4, 64, FAKE), -3),   # B*H = 65536 > 65535
     ((0, 1, 1, 8, 4, 4, 4, 64, NULL), -1),       # null tensors
 ])
 def test_prefill_validation(lib, args, code):
@@ -85,6 +89,10 @@ def test_decode_and_feature_map_validation(lib):
     assert lib.sata_decode_step(NULL, FAKE, FAKE, FAKE, 0, 1, 1, 4, 4, 4, FAKE, NULL) == -1
     assert lib.sata_decode_step(FAKE, FAKE, FAKE, FAKE, 3, 1, 1, 4, 4, 4, FAKE, NULL) == -1
     assert lib.sata_decode_step(FAKE, FAKE, FAKE, FAKE, 0, 1, 1, 4, 4, 0, FAKE, NULL) == -1
+    assert lib.sata_decode_step(FAKE, FAKE, FAKE, FAKE, 0, 1, 1, 256, 4, 2, FAKE, NULL) == -1
+    assert lib.sata_decode_step(FAKE, FAKE, FAKE, FAKE, 0, 1, 1, 4, 256, 2, FAKE, NULL) == -1
+    assert lib.sata_decode_step(FAKE, FAKE, FAKE, FAKE, 0, 256, 256, 4, 4, 4, FAKE, NULL) == -3
+    assert lib.sata_feature_map(FAKE, 0, 3, 256, 2, FAKE, NULL) == -1
     assert lib.sata_feature_map(FAKE, 0, -5, 4, 3, FAKE, NULL) == -1
     assert lib.sata_feature_map(FAKE, 0, 0, 4, 3, FAKE, NULL) == 0   # rows = 0: no-op
     assert lib.sata_feature_map(NULL, 0, 3, 4, 3, FAKE, NULL) == -1
