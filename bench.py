@@ -24,7 +24,13 @@ its own line in the same form:
   large_d64   B=2, H=8, d_k=d_v=64, P=4 (D=47905), bf16: 4096-token prefill,
               then 1024 decode steps;
   sweep_d16   B=1, H=64, d_k=d_v=16, float32, n=65536: prefill for each P in
-              2..6 (the CPU leg also reports the error against softmax).
+              2..6 (the CPU leg also reports the error against softmax);
+  error_study one head of 100,000 tokens, float32, for each d_k = d_v in
+              {8, 16, 32} with P = 1..6 and d = 64 with P = 1..5: the
+              prefill is timed, and the CPU leg measures its output against
+              exact float64 softmax attention on sampled rows, overall and by
+              token position, in decimal orders of magnitude of the elementwise
+              absolute difference (the reconstruction measure of App. A3-A4).
 """
 from __future__ import annotations
 
@@ -101,7 +107,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-heads", type=int, default=48)
     ap.add_argument("--cpu-sample-decode-rows", type=int, default=128)
-    ap.add_argument("--workload", default="headline", choices=["headline", "decode_d16", "large_d64", "sweep_d16"])
+    ap.add_argument("--workload", default="headline", choices=["headline", "decode_d16", "large_d64", "sweep_d16",
+                                                                  "error_study"])
+    ap.add_argument("--seq-len", type=int, default=0,
+                    help="error_study only: tokens per sequence (default 100000)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before timing, run one device-to-device copy of this many MiB (a kernel of "
                          "known traffic for calibrating hardware byte counters)")
@@ -312,6 +321,113 @@ def cpu_baseline_workload(wid, Bw, Hw, n, d, Ps, dt, y_gpu, pre, sata, torch):
     return out
 
 
+ERROR_STUDY_CELLS = [(d, p) for d in (8, 16, 32) for p in range(1, 7)] + [(64, p) for p in range(1, 6)]
+ERROR_STUDY_N = 100_000
+
+
+def error_study_rows(n):
+    """Query rows the error study samples: log-spaced over the positions (so
+    that every decade of context is represented) plus uniformly drawn ones."""
+    import numpy as np
+    logr = np.unique(np.round(np.logspace(0, math.log10(n), 96)).astype(np.int64) - 1)
+    uni = np.random.default_rng(2602).integers(0, n, 64)
+    return sorted(set(int(r) for r in logr if 0 <= r < n) | set(int(r) for r in uni))
+
+
+def run_error_study(args, sata, torch):
+    """Prefill of one 100K-token head per (d, P) cell, timed; the CPU leg
+    compares the outputs with exact softmax attention (App. A3-A4)."""
+    import numpy as np
+
+    import sata_synth as syn
+    n = args.seq_len or ERROR_STUDY_N
+    cells, outs = {}, {}
+    t_total = 0.0
+    for d, Pw in ERROR_STUDY_CELLS:
+        q, k, v = syn.make_head(600 + d, 0, 0, n, d, d, "f32")
+        dev = [torch.from_numpy(a).to("cuda").view(1, 1, n, d) for a in (q, k, v)]
+        y = torch.empty(1, 1, n, d, dtype=torch.float32, device="cuda")
+        S = torch.empty(1, 1, feature_count(d, Pw), d + 1, dtype=torch.float32, device="cuda")
+        for _ in range(args.warmup):
+            sata.prefill(*dev, Pw, CHUNK, y=y, S=S)
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        ev[0].record()
+        for s_ in range(args.steps):
+            sata.prefill(*dev, Pw, CHUNK, y=y, S=S)
+            ev[s_ + 1].record()
+        torch.cuda.synchronize()
+        ms = ev[0].elapsed_time(ev[-1]) / args.steps
+        t_total += ms
+        flops = prefill_flops_per_head_token(d, d, Pw, CHUNK) * n
+        ach = flops / (ms * 1e-3) / 1e12
+        cells[f"d{d}_P{Pw}"] = {
+            "d": d, "P": Pw, "D": feature_count(d, Pw), "prefill_ms": ms, "prefill_tokens_per_s": n / (ms * 1e-3),
+            "prefill_roofline": {"kernel": "sata_prefill (all launches of one call)", "bound": "alu",
+                                 "achieved": ach, "peak": PEAK_F32_TFLOPS, "unit": "TFLOP/s",
+                                 "frac": ach / PEAK_F32_TFLOPS, "traffic": None, "work_per_launch": flops}}
+        outs[(d, Pw)] = y[0, 0].cpu().numpy()
+        del dev, y, S
+    worst = min(cells.values(), key=lambda c: c["prefill_roofline"]["frac"])
+    line = {
+        "metric": "prefill tokens/s + decode tokens/s (d_k=32,P=4); % MFMA/HBM roofline",
+        "value": n * len(cells) / (t_total * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": t_total, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": (f"error_study: causal prefill of one head, n={n}, float32, chunk={CHUNK}, "
+                                f"for d_k=d_v in 8/16/32 with P=1..6 and 64 with P=1..5"),
+                   "global_batch": 1, "seq_len": n, "decode_steps": 0, "heads": 1, "chunk": CHUNK,
+                   "parallelism": "single GPU"},
+        "cells": cells,
+        "roofline": worst["prefill_roofline"],
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline_error_study(n, outs)
+    return line
+
+
+def cpu_baseline_error_study(n, outs):
+    """Per cell, on the sampled rows: the GPU output against the float64 oracle
+    (parity), and both against exact float64 softmax attention as
+    log10 |difference| per output element: median, 99th percentile and maximum
+    overall, and the median per decade of token position."""
+    import numpy as np
+
+    import oracle
+    import sata_synth as syn
+    threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    rows = error_study_rows(n)
+    pos = np.asarray(rows)
+    decades = [(0, 10), (10, 100), (100, 1000), (1000, 10000), (10000, n)]
+    summary = lambda a: {"median": float(np.median(a)), "p99": float(np.percentile(a, 99)), "max": float(a.max())}
+    per_cell = {}
+    t = 0.0
+    soft = {}
+    for (d, Pw), y_gpu in outs.items():
+        q, k, v = syn.make_head(600 + d, 0, 0, n, d, d, "f32")
+        if d not in soft:
+            soft[d] = oracle.softmax_attention_rows(q, k, v, rows)
+        t0 = time.perf_counter()
+        yr, _, kap = oracle.taylor_attention_rows(q, k, v, Pw, rows)
+        t += time.perf_counter() - t0
+        lg = oracle.log10_abs_diff(y_gpu[rows], soft[d])
+        lo = oracle.log10_abs_diff(yr, soft[d])
+        by_pos = {}
+        for lo_, hi_ in decades:
+            m = (pos >= lo_) & (pos < hi_)
+            if m.any():
+                by_pos[f"{lo_}-{hi_ - 1}"] = float(np.median(lg[m]))
+        per_cell[f"d{d}_P{Pw}"] = {
+            "parity_max_row_rel_err": oracle.max_row_rel_error(y_gpu[rows], yr, kap)[0],
+            "gpu_vs_softmax_log10": summary(lg.ravel()),
+            "oracle_vs_softmax_log10": summary(lo.ravel()),
+            "gpu_vs_softmax_median_log10_by_position": by_pos}
+    return {"value": len(outs) * len(rows) / t, "unit": "rows/s", "cores": threads, "kind": "oracle",
+            "sample": (f"{len(rows)} query rows (96 log-spaced positions and 64 uniform ones) of each cell's "
+                       f"{n}-token head, direct float64 definition; the softmax reference on the same rows"),
+            "seconds": t, "per_cell": per_cell}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -325,6 +441,9 @@ def main():
     import paper_2602_00294_amd as sata
     sata.load_library()
     assert torch.cuda.is_available(), "no GPU"
+    if args.workload == "error_study":
+        print(json.dumps(run_error_study(args, sata, torch)), flush=True)
+        return
     if args.workload != "headline":
         print(json.dumps(run_workload(args, sata, torch)), flush=True)
         return
