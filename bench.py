@@ -30,7 +30,13 @@ its own line in the same form:
               prefill is timed, and the CPU leg measures its output against
               exact float64 softmax attention on sampled rows, overall and by
               token position, in decimal orders of magnitude of the elementwise
-              absolute difference (the reconstruction measure of App. A3-A4).
+              absolute difference (the reconstruction measure of App. A3-A4);
+  context_sweep one head per head size d_k = d_v in {8, 16, 32} with
+              contexts of 10^3 ... 10^8 tokens (d = 64: up to 10^7), float32,
+              P = 4: prefill time and device memory per token, then 64 decode
+              steps (per-step time), and the CPU leg checks decoded rows at the
+              longest context, far beyond 2^24 tokens, against the oracle
+              (Sec. 3.2: cost per token that does not grow with the context).
 """
 from __future__ import annotations
 
@@ -108,7 +114,7 @@ def parse():
     ap.add_argument("--cpu-sample-heads", type=int, default=48)
     ap.add_argument("--cpu-sample-decode-rows", type=int, default=128)
     ap.add_argument("--workload", default="headline", choices=["headline", "decode_d16", "large_d64", "sweep_d16",
-                                                                  "error_study"])
+                                                                  "error_study", "context_sweep"])
     ap.add_argument("--seq-len", type=int, default=0,
                     help="error_study only: tokens per sequence (default 100000)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -428,6 +434,108 @@ def cpu_baseline_error_study(n, outs):
             "seconds": t, "per_cell": per_cell}
 
 
+CONTEXT_SWEEP = [(8, 8), (16, 8), (32, 8), (64, 7)]  # (d, largest power of ten of the context)
+CONTEXT_DECODE = 64
+
+
+def run_context_sweep(args, sata, torch):
+    """Prefill of contexts 10^3 ... 10^8 tokens, then decode steps, per head
+    size; time and device memory per token.  Inputs: sata_synth.long_head."""
+    import numpy as np
+
+    import sata_synth as syn
+    Pw = 4
+    cells = {}
+    keep = {}
+    t_total = 0.0
+    for d, emax in CONTEXT_SWEEP:
+        n_max = 10 ** emax
+        q, k, v = syn.long_head(700 + d, n_max + CONTEXT_DECODE, d, d)
+        for e in range(3, emax + 1):
+            T = 10 ** e
+            torch.cuda.synchronize()
+            sata.release()  # so that what the library holds afterwards is this call's own
+            torch.cuda.reset_peak_memory_stats()
+            free0 = torch.cuda.mem_get_info()[0]
+            base = torch.cuda.memory_allocated()
+            res0 = torch.cuda.memory_reserved()
+            dev = [torch.from_numpy(a[:T]).to("cuda").view(1, 1, T, d) for a in (q, k, v)]
+            y = torch.empty(1, 1, T, d, dtype=torch.float32, device="cuda")
+            S = torch.empty(1, 1, feature_count(d, Pw), d + 1, dtype=torch.float32, device="cuda")
+            dq, dk_, dv_ = (torch.from_numpy(np.ascontiguousarray(a[T:T + CONTEXT_DECODE])).to("cuda")
+                            .view(CONTEXT_DECODE, 1, 1, d) for a in (q, k, v))
+            ydec = torch.empty(CONTEXT_DECODE, 1, 1, d, dtype=torch.float32, device="cuda")
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            torch.cuda.synchronize()
+            ev[0].record()
+            sata.prefill(*dev, Pw, CHUNK, y=y, S=S)
+            ev[1].record()
+            for t in range(CONTEXT_DECODE):
+                sata.decode_step(S, dq[t], dk_[t], dv_[t], Pw, y=ydec[t])
+            ev[2].record()
+            torch.cuda.synchronize()
+            pre_ms = ev[0].elapsed_time(ev[1])
+            dec_ms = ev[1].elapsed_time(ev[2]) / CONTEXT_DECODE
+            # device memory: what torch allocated for the call (inputs, outputs,
+            # state) plus what the library holds (tables, workspace), read from
+            # the device's free memory
+            torch_peak = torch.cuda.max_memory_allocated() - base
+            lib_held = max(0, (free0 - torch.cuda.mem_get_info()[0]) - (torch.cuda.memory_reserved() - res0))
+            t_total += pre_ms + dec_ms * CONTEXT_DECODE
+            cells[f"d{d}_T{T}"] = {
+                "d": d, "context": T, "prefill_ms": pre_ms, "prefill_ns_per_token": pre_ms * 1e6 / T,
+                "decode_us_per_step": dec_ms * 1e3, "state_bytes": S.numel() * 4,
+                "device_bytes_peak": int(torch_peak + lib_held),
+                "device_bytes_per_token": (torch_peak + lib_held) / T}
+            print(f"context d={d} T={T}: prefill {pre_ms:.1f} ms, decode {dec_ms * 1e3:.1f} us/step",
+                  file=sys.stderr, flush=True)
+            if e == emax:
+                keep[d] = ydec[:, 0, 0].cpu().numpy()
+            del dev, y, S, dq, dk_, dv_, ydec
+            torch.cuda.empty_cache()
+        del q, k, v
+    line = {
+        "metric": "prefill tokens/s + decode tokens/s (d_k=32,P=4); % MFMA/HBM roofline",
+        "value": sum(c["context"] + CONTEXT_DECODE for c in cells.values()) / (t_total * 1e-3),
+        "unit": "tokens/s", "n_gpus": 1, "steps": 1, "warmup": 0, "ms_per_step": t_total,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": (f"context_sweep: one head, float32, P={Pw}, chunk={CHUNK}: prefill of 10^3..10^8 "
+                                f"tokens (d=64: ..10^7) then {CONTEXT_DECODE} decode steps, d_k=d_v in 8/16/32/64"),
+                   "global_batch": 1, "seq_len": 10 ** 8, "decode_steps": CONTEXT_DECODE, "heads": 1, "P": Pw,
+                   "chunk": CHUNK, "parallelism": "single GPU"},
+        "cells": cells,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline_context(keep, Pw)
+    return line
+
+
+def cpu_baseline_context(keep, Pw):
+    """The oracle at the longest context of each head size: decoded rows
+    0, 31 and 63 (positions just past 10^emax), direct float64 definition."""
+    import numpy as np
+
+    import oracle
+    import sata_synth as syn
+    threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    out, t = {}, 0.0
+    for d, emax in CONTEXT_SWEEP:
+        n_max = 10 ** emax
+        q, k, v = syn.long_head(700 + d, n_max + CONTEXT_DECODE, d, d)
+        steps = [0, CONTEXT_DECODE // 2 - 1, CONTEXT_DECODE - 1]
+        print(f"oracle d={d} T={n_max}", file=sys.stderr, flush=True)
+        t0 = time.perf_counter()
+        yr, _, kap = oracle.taylor_attention_rows(q, k, v, Pw, [n_max + s for s in steps])
+        t += time.perf_counter() - t0
+        out[f"d{d}_T{n_max}"] = {"decode_rows": steps,
+                                 "max_row_rel_err": oracle.max_row_rel_error(keep[d][steps], yr, kap)[0]}
+        del q, k, v
+    return {"value": sum(3 * (10 ** e + CONTEXT_DECODE) for _, e in CONTEXT_SWEEP) / t, "unit": "keys/s",
+            "cores": threads, "kind": "oracle",
+            "sample": "3 decoded rows after the longest context of each head size, direct float64 definition",
+            "seconds": t, "parity": out}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -441,6 +549,9 @@ def main():
     import paper_2602_00294_amd as sata
     sata.load_library()
     assert torch.cuda.is_available(), "no GPU"
+    if args.workload == "context_sweep":
+        print(json.dumps(run_context_sweep(args, sata, torch)), flush=True)
+        return
     if args.workload == "error_study":
         print(json.dumps(run_error_study(args, sata, torch)), flush=True)
         return

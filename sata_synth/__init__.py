@@ -10,6 +10,12 @@ can be regenerated alone.  Values are drawn in float64, rounded to float32
 (round to nearest even) and, for bf16 workloads, from float32 to bfloat16
 (round to nearest even).  The arrays returned are float32 holding exactly the
 values that the GPU receives, so the oracle sees the same inputs bit for bit.
+
+Long sequences (``long_head``, up to 10^8 tokens) are drawn faster: float32
+N(0, 1) values straight from the generator, in blocks of 2^20 tokens, each
+block from its own stream ``default_rng([SEED, workload, LONG, block,
+tensor])``, so that the blocks can be drawn in parallel threads and any
+prefix of the sequence is the same whatever its length.
 """
 from __future__ import annotations
 
@@ -17,8 +23,10 @@ import numpy as np
 
 SEED = 260200294
 TENSOR_Q, TENSOR_K, TENSOR_V = 0, 1, 2
+LONG = 1 << 20  # stream-key tag of the long-sequence generator
+LONG_BLOCK = 1 << 20  # tokens per block
 
-__all__ = ["SEED", "round_to_bf16", "bf16_bits", "head_stream", "make_qkv", "make_head"]
+__all__ = ["SEED", "round_to_bf16", "bf16_bits", "head_stream", "make_qkv", "make_head", "long_head"]
 
 
 def round_to_bf16(x) -> np.ndarray:
@@ -66,3 +74,21 @@ def make_qkv(workload: int, B: int, H: int, n: int, d_k: int, d_v: int, dtype: s
         for h in range(H):
             q[b, h], k[b, h], v[b, h] = make_head(workload, b, h, n, d_k, d_v, dtype)
     return q, k, v
+
+
+def long_head(workload: int, n: int, d_k: int, d_v: int, threads: int = 16):
+    """(q [n, d_k], k [n, d_k], v [n, d_v]) float32 N(0, 1) for one long head;
+    blocks of LONG_BLOCK tokens drawn in parallel threads."""
+    from concurrent.futures import ThreadPoolExecutor
+    out = [np.empty((n, d_k), np.float32), np.empty((n, d_k), np.float32), np.empty((n, d_v), np.float32)]
+    jobs = [(t, b) for t in range(3) for b in range((n + LONG_BLOCK - 1) // LONG_BLOCK)]
+
+    def fill(job):
+        t, b = job
+        r0, r1 = b * LONG_BLOCK, min(n, (b + 1) * LONG_BLOCK)
+        rng = np.random.default_rng([SEED, int(workload), LONG, b, t])
+        out[t][r0:r1] = rng.standard_normal((r1 - r0, out[t].shape[1]), dtype=np.float32)
+
+    with ThreadPoolExecutor(max(1, threads)) as ex:
+        list(ex.map(fill, jobs))
+    return tuple(out)

@@ -10,6 +10,8 @@ benchmark times, checked on sampled outputs the oracle computes one by one.
 * d_k = d_v = 8, P = 4, float32: one head, n=256, every row and the state.
 * d_k = d_v = 8, float32, one head of 100,000 tokens, P = 1..6: parity and the
   fall of the error against softmax attention with each Taylor term.
+* d_k = d_v = 8, P = 4, float32, one head of 2^25 + 4096 tokens: the last
+  prefill rows and 4 decode steps after them.
 
 Rows compared: the first and last rows of chunks near the start, the middle
 and the end, plus seeded random rows; heads: the first, the last and a
@@ -169,3 +171,29 @@ def test_reconstruction_error_falls_with_each_term(sata):
         medians.append(float(np.median(oracle.log10_abs_diff(yg, soft))))
     _say(f"median log10 |y - softmax| for P=1..6: {[round(m, 2) for m in medians]}")
     assert all(b < a for a, b in zip(medians, medians[1:])), medians
+
+
+def test_float32_state_beyond_2_pow_24_tokens(sata):
+    """A context longer than float32 counts exactly (2^25 + 4096 tokens, d = 8,
+    P = 4, float32): the normaliser column outgrows the float32 integer range,
+    yet the last prefill rows and the decoded rows after it stay within the
+    float32 tolerance of the oracle."""
+    n, d, P, steps = (1 << 25) + 4096, 8, 4, 4
+    _say(f"long context n={n}")
+    q, k, v = syn.long_head(708, n + steps, d, d)
+    dev = [torch.from_numpy(a[:n]).to("cuda").view(1, 1, n, d) for a in (q, k, v)]
+    y, S = sata.prefill(*dev, P, 64)
+    torch.cuda.synchronize()
+    rows = [n - 4096, n - 1]
+    yg = y[0, 0, rows].cpu().numpy()
+    del dev, y
+    ys = []
+    for t in range(n, n + steps):
+        step = [torch.from_numpy(a[t:t + 1]).to("cuda").view(1, 1, d) for a in (q, k, v)]
+        ys.append(sata.decode_step(S, *step, P)[0, 0].cpu().numpy())
+    _say("oracle rows")
+    yr, _, kap = oracle.taylor_attention_rows(q, k, v, P, rows + list(range(n, n + steps)))
+    got = np.concatenate([yg, np.stack(ys)]).astype(np.float64)
+    err, _ = max_row_rel_error(got, yr, kap)
+    _say(f"worst row error after {n} tokens: {err:.3e}")
+    assert err <= TOL["f32"], err
