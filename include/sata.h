@@ -111,6 +111,25 @@ sata_status sata_decode_step(float* S, const void* q, const void* k, const void*
                              sata_dtype dt, int B, int H, int d_k, int d_v, int P,
                              void* y, void* stream);
 
+/* One decode step with grouped query heads: each of the B*H_kv key/value
+ * heads keeps one state and serves G consecutive query heads (query head
+ * g + G*h reads key/value head h).  Sharing one key/value head among several
+ * query heads is among the reuse schemes that a footnote of Sec. 3.3 says carry
+ * over to this formulation; the update and readout are those of
+ * sata_decode_step (App. A2), with the readout done for every query head:
+ *   S += phi(k_h) (x) [v_h, 1];  y_{g+G h} = (phi(q_{g+G h})^T S)[0:d_v] / (...)[d_v]
+ *   S    : [B][H_kv][D][d_v+1] float32 (device, read and written in place;
+ *          16-byte aligned for G > 1)
+ *   q    : [B][H_kv*G][d_k], k : [B][H_kv][d_k], v : [B][H_kv][d_v], dtype dt
+ *   y    : [B][H_kv*G][d_v], dtype dt (device, written)
+ * G = 1 is sata_decode_step.  G in {2, 4, 8} streams each state once for its
+ * G query heads; other G, d_v large enough that no plan fits on chip (at
+ * most 127 for large heads), or an unaligned state give SATA_ERR_UNSUPPORTED.
+ * B*H_kv*G <= 65535. */
+sata_status sata_decode_step_grouped(float* S, const void* q, const void* k, const void* v,
+                                     sata_dtype dt, int B, int H_kv, int G, int d_k, int d_v, int P,
+                                     void* y, void* stream);
+
 /* Static text for a status code. */
 const char* sata_status_string(sata_status s);
 

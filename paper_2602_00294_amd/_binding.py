@@ -50,6 +50,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.sata_prefill.restype = i32
     lib.sata_decode_step.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp]
     lib.sata_decode_step.restype = i32
+    lib.sata_decode_step_grouped.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp, vp]
+    lib.sata_decode_step_grouped.restype = i32
     lib.sata_status_string.argtypes = [i32]
     lib.sata_status_string.restype = ctypes.c_char_p
     lib.sata_last_error.argtypes = []
@@ -187,6 +189,34 @@ def decode_step(S, q, k, v, P: int, y=None):
     _check_tensor(y, "y")
     _check(load_library().sata_decode_step(_ptr(S), _ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, H, dk, dv, P,
                                            _ptr(y), _stream_ptr()), "sata_decode_step")
+    return y
+
+
+def decode_step_grouped(S, q, k, v, P: int, y=None):
+    """One decode step with grouped query heads, in place on S [B, H_kv, D, d_v+1].
+
+    q: [B, H_q, d_k] with H_q = G * H_kv (query head g + G*h reads key/value
+    head h); k: [B, H_kv, d_k]; v: [B, H_kv, d_v].  Returns y [B, H_q, d_v].
+    """
+    torch = _torch()
+    for name, t in (("S", S), ("q", q), ("k", k), ("v", v)):
+        _check_tensor(t, name)
+    if S.dtype != torch.float32:
+        raise TypeError("S must be float32")
+    B, Hq, dk = q.shape
+    Hkv = k.shape[1]
+    dv = v.shape[-1]
+    if tuple(k.shape) != (B, Hkv, dk) or tuple(v.shape[:2]) != (B, Hkv) or Hq % Hkv:
+        raise ValueError("q [B, G*H_kv, d_k], k [B, H_kv, d_k], v [B, H_kv, d_v] expected")
+    G = Hq // Hkv
+    D = feature_count(dk, P)
+    if tuple(S.shape) != (B, Hkv, D, dv + 1):
+        raise ValueError(f"S must be [B, H_kv, {D}, {dv + 1}]")
+    if y is None:
+        y = torch.empty(B, Hq, dv, dtype=q.dtype, device=q.device)
+    _check_tensor(y, "y")
+    _check(load_library().sata_decode_step_grouped(_ptr(S), _ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, Hkv, G,
+                                                   dk, dv, P, _ptr(y), _stream_ptr()), "sata_decode_step_grouped")
     return y
 
 

@@ -39,6 +39,23 @@ hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, 
                          int BH, int dk, int dv, const DevTable& t, const DecodePlan& plan,
                          float* partial, int* counters, hipStream_t s);
 
+// ---- decode step, grouped query heads ------------------------------------------
+struct GroupedDecodePlan {
+  int tu = 0;      // > 0: supported; threads of the workgroup taking part in the stream
+  size_t lds = 0;
+  int nth = 1024;  // threads per workgroup (256 or 1024)
+  int np = 1;      // workgroups (pieces) per key/value head
+  int steps = 0;   // float4 steps per thread over a whole head
+  int rows = 0;    // state rows a piece touches at most
+  int G = 0;       // query heads per key/value head (2, 4 or 8)
+};
+GroupedDecodePlan plan_decode_grouped(int64_t D, int dk, int dv, int BH, int G);
+// BH key/value heads; S 16-byte aligned; partial: BH * np * G * (dv + 1)
+// floats and counters: BH ints, all zero, when np > 1.
+hipError_t launch_decode_grouped(float* S, const void* q, const void* k, const void* v, void* y, bool bf16,
+                                 int BH, int dk, int dv, const DevTable& t, const GroupedDecodePlan& plan,
+                                 float* partial, int* counters, hipStream_t s);
+
 // ---- prefill, generic float32 path --------------------------------------------
 struct PrefillGenericPlan {
   int fs = 0;        // features per slice

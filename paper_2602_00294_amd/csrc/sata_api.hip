@@ -321,6 +321,43 @@ sata_status sata_decode_step(float* S, const void* q, const void* k, const void*
   return ok();
 }
 
+sata_status sata_decode_step_grouped(float* S, const void* q, const void* k, const void* v, sata_dtype dt, int B,
+                                     int H_kv, int G, int d_k, int d_v, int P, void* y, void* stream) {
+  if (!valid_dtype(dt)) return fail(SATA_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
+  if (B < 1 || H_kv < 1) return fail(SATA_ERR_INVALID_ARG, "B=%d H_kv=%d must be >= 1", B, H_kv);
+  if (G < 1) return fail(SATA_ERR_INVALID_ARG, "G=%d must be >= 1", G);
+  int64_t D = 0;
+  sata_status st = check_dims(d_k, d_v, P, &D);
+  if (st != SATA_OK) return st;
+  if ((int64_t)B * H_kv * G > kMaxHeads)
+    return fail(SATA_ERR_TOO_LARGE, "B*H_kv*G=%lld exceeds %d", (long long)B * H_kv * G, kMaxHeads);
+  if (!S || !q || !k || !v || !y) return fail(SATA_ERR_INVALID_ARG, "null tensor pointer");
+  if (G == 1) return sata_decode_step(S, q, k, v, dt, B, H_kv, d_k, d_v, P, y, stream);
+  if (G != 2 && G != 4 && G != 8) return fail(SATA_ERR_UNSUPPORTED, "G=%d; supported: 1, 2, 4, 8", G);
+  if (((uintptr_t)S & 15) != 0) return fail(SATA_ERR_UNSUPPORTED, "grouped decode needs a 16-byte aligned state");
+  const int BH = B * H_kv;
+  sata::GroupedDecodePlan plan = sata::plan_decode_grouped(D, d_k, d_v, BH, G);
+  if (plan.tu <= 0)
+    return fail(SATA_ERR_UNSUPPORTED, "no grouped decode plan fits on chip for d_k=%d d_v=%d P=%d G=%d", d_k, d_v, P,
+                G);
+  hipStream_t s = (hipStream_t)stream;
+  sata::DevTable t;
+  if ((st = get_table(d_k, P, s, &t)) != SATA_OK) return st;
+  float* partial = nullptr;
+  int* counters = nullptr;
+  if (plan.np > 1) {
+    void* ws = nullptr;
+    const size_t bytes = sizeof(float) * (size_t)BH * plan.np * G * (d_v + 1);
+    if ((st = get_workspace(bytes, s, &ws)) != SATA_OK) return st;
+    partial = (float*)ws;
+    if ((st = get_counters(BH, s, &counters)) != SATA_OK) return st;
+  }
+  hipError_t e = sata::launch_decode_grouped(S, q, k, v, y, dt == SATA_BF16, BH, d_k, d_v, t, plan, partial,
+                                             counters, s);
+  if (e != hipSuccess) return hip_fail(e, "grouped decode launch");
+  return ok();
+}
+
 const char* sata_status_string(sata_status s) {
   switch (s) {
     case SATA_OK: return "ok";

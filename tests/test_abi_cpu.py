@@ -93,6 +93,15 @@ def test_decode_and_feature_map_validation(lib):
     assert lib.sata_decode_step(FAKE, FAKE, FAKE, FAKE, 0, 1, 1, 4, 256, 2, FAKE, NULL) == -1
     assert lib.sata_decode_step(FAKE, FAKE, FAKE, FAKE, 0, 256, 256, 4, 4, 4, FAKE, NULL) == -3
     assert lib.sata_feature_map(FAKE, 0, 3, 256, 2, FAKE, NULL) == -1
+    # grouped decode: (S, q, k, v, dtype, B, H_kv, G, d_k, d_v, P, y, stream)
+    g = lib.sata_decode_step_grouped
+    assert g(FAKE, FAKE, FAKE, FAKE, 0, 1, 1, 0, 4, 4, 4, FAKE, NULL) == -1       # G = 0
+    assert g(NULL, FAKE, FAKE, FAKE, 0, 1, 1, 4, 4, 4, 4, FAKE, NULL) == -1       # null state
+    assert g(FAKE, FAKE, FAKE, FAKE, 0, 1, 1, 3, 4, 4, 4, FAKE, NULL) == -2       # G = 3
+    assert g(FAKE, FAKE, FAKE, FAKE, 0, 1, 1, 16, 4, 4, 4, FAKE, NULL) == -2      # G = 16
+    assert g(ctypes.c_void_p(0x1004), FAKE, FAKE, FAKE, 0, 1, 1, 4, 4, 4, 4, FAKE, NULL) == -2  # unaligned
+    assert g(FAKE, FAKE, FAKE, FAKE, 0, 1, 1, 4, 4, 200, 4, FAKE, NULL) == -2     # d_v = 200: no plan
+    assert g(FAKE, FAKE, FAKE, FAKE, 0, 64, 128, 8, 4, 4, 4, FAKE, NULL) == -3    # B*H_kv*G = 65536
     assert lib.sata_feature_map(FAKE, 0, -5, 4, 3, FAKE, NULL) == -1
     assert lib.sata_feature_map(FAKE, 0, 0, 4, 3, FAKE, NULL) == 0   # rows = 0: no-op
     assert lib.sata_feature_map(NULL, 0, 3, 4, 3, FAKE, NULL) == -1

@@ -1,0 +1,95 @@
+"""GPU parity of the grouped-query decode (sata_decode_step_grouped): each
+key/value head keeps one state and serves G query heads.  The reference is
+the float64 oracle applied per query head to its key/value head's tokens
+(query head g + G h reads key/value head h); the state must equal the
+oracle's state of the key/value head."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import sata_synth as syn
+from gpu_util import TOL, to_dev, to_host
+from oracle.metrics import max_row_rel_error, state_rel_error
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def sata():
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    import paper_2602_00294_amd as m
+    m.load_library()
+    return m
+
+
+def _say(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def _inputs(wid, B, Hkv, G, n, d, dtype):
+    q, _, _ = syn.make_qkv(wid, B, Hkv * G, n, d, d, dtype)
+    _, k, v = syn.make_qkv(wid + 1, B, Hkv, n, d, d, dtype)
+    return q, k, v
+
+
+def _state_after_prefill(sata, k, v, n1, P, dtype):
+    B, Hkv, _, d = k.shape
+    if n1 == 0:
+        return torch.zeros(B, Hkv, oracle.feature_count(d, P), v.shape[-1] + 1, device="cuda")
+    kk = to_dev(k[:, :, :n1], dtype)
+    _, S = sata.prefill(kk, kk, to_dev(v[:, :, :n1], dtype), P, 32)  # the state does not depend on q
+    return S
+
+
+@pytest.mark.parametrize("B,Hkv,G,n1,n2,d,P,dtype", [
+    (1, 2, 4, 40, 3, 8, 4, "f32"),     # small heads: one 256-thread workgroup per head
+    (2, 3, 2, 70, 2, 16, 4, "bf16"),
+    (1, 2, 8, 30, 2, 32, 4, "bf16"),   # the benchmark's head size, several pieces per head
+    (1, 1, 4, 20, 2, 64, 4, "f32"),    # D = 47905: many pieces per head
+    (1, 2, 2, 0, 3, 5, 3, "f32"),      # empty prefill; rows of 6 floats, heads not 16-byte aligned
+    (2, 4, 4, 10, 2, 7, 5, "f32"),
+])
+def test_grouped_decode_matches_oracle(sata, B, Hkv, G, n1, n2, d, P, dtype):
+    _say(f"grouped decode B={B} H_kv={Hkv} G={G} n1={n1} n2={n2} d={d} P={P} {dtype}")
+    q, k, v = _inputs(80 + d, B, Hkv, G, n1 + n2, d, dtype)
+    S = _state_after_prefill(sata, k, v, n1, P, dtype)
+    ys = []
+    for t in range(n1, n1 + n2):
+        ys.append(to_host(sata.decode_step_grouped(S, to_dev(q[:, :, t].copy(), dtype), to_dev(k[:, :, t].copy(), dtype),
+                                                   to_dev(v[:, :, t].copy(), dtype), P)))
+    torch.cuda.synchronize()
+    S_host = to_host(S)
+    for b in range(B):
+        for hq in range(Hkv * G):
+            h = hq // G
+            yr, _, kap = oracle.taylor_attention_rows(q[b, hq], k[b, h], v[b, h], P, list(range(n1, n1 + n2)))
+            got = np.stack([yy[b, hq] for yy in ys])
+            err, _ = max_row_rel_error(got, yr, kap)
+            assert err <= TOL[dtype], f"b{b} query head {hq}: {err:.3e}"
+        for h in range(Hkv):
+            s_err = state_rel_error(S_host[b, h], oracle.state_ref(k[b, h], v[b, h], P))
+            assert s_err <= TOL[dtype], f"state b{b} h{h}: {s_err:.3e}"
+
+
+def test_grouped_decode_deterministic_and_g1_is_decode_step(sata):
+    """Repeated calls give identical bits; G = 1 is the single-query decode."""
+    B, Hkv, G, n, d, P = 1, 2, 4, 50, 32, 4
+    q, k, v = _inputs(90, B, Hkv, G, n + 1, d, "bf16")
+    S0 = _state_after_prefill(sata, k, v, n, P, "bf16")
+    step = [to_dev(a[:, :, n].copy(), "bf16") for a in (q, k, v)]
+    S1, S2 = S0.clone(), S0.clone()
+    y1 = sata.decode_step_grouped(S1, *step, P)
+    y2 = sata.decode_step_grouped(S2, *step, P)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2) and torch.equal(S1, S2)
+    q1 = step[0][:, ::G].contiguous()  # one query head per key/value head
+    S3, S4 = S0.clone(), S0.clone()
+    ya = sata.decode_step_grouped(S3, q1, step[1], step[2], P)
+    yb = sata.decode_step(S4, q1, step[1], step[2], P)
+    torch.cuda.synchronize()
+    assert torch.equal(ya, yb) and torch.equal(S3, S4)
