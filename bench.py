@@ -36,7 +36,12 @@ its own line in the same form:
               P = 4: prefill time and device memory per token, then 64 decode
               steps (per-step time), and the CPU leg checks decoded rows at the
               longest context, far beyond 2^24 tokens, against the oracle
-              (Sec. 3.2: cost per token that does not grow with the context).
+              (Sec. 3.2: cost per token that does not grow with the context);
+  decode_grouped B=8, 32 query heads, d_k=d_v=32, P=4, bf16: an 8192-token
+              prefill of the key/value heads, then 1024 grouped decode steps
+              for G = 2, 4, 8 query heads per key/value head (16, 8, 4
+              key/value heads); one state read per key/value head serves its
+              G query heads.
 """
 from __future__ import annotations
 
@@ -114,7 +119,8 @@ def parse():
     ap.add_argument("--cpu-sample-heads", type=int, default=48)
     ap.add_argument("--cpu-sample-decode-rows", type=int, default=128)
     ap.add_argument("--workload", default="headline", choices=["headline", "decode_d16", "large_d64", "sweep_d16",
-                                                                  "error_study", "context_sweep"])
+                                                                  "error_study", "context_sweep",
+                                                                  "decode_grouped"])
     ap.add_argument("--seq-len", type=int, default=0,
                     help="error_study only: tokens per sequence (default 100000)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -434,6 +440,85 @@ def cpu_baseline_error_study(n, outs):
             "seconds": t, "per_cell": per_cell}
 
 
+GROUPED_QUERY_HEADS = 32
+GROUPED_GS = [2, 4, 8]
+
+
+def run_decode_grouped(args, sata, torch):
+    """Grouped-query decode at the headline head size: prefill the key/value
+    heads, then time the decode steps for each G; returns the JSON line."""
+    import numpy as np
+
+    import sata_synth as syn
+    n_dec = args.decode_steps
+    per_G = {}
+    t_total = 0.0
+    roof = None
+    for G in GROUPED_GS:
+        Hkv = GROUPED_QUERY_HEADS // G
+        q = np.empty((B, GROUPED_QUERY_HEADS, n_dec, DK), np.float32)
+        for b in range(B):
+            for h in range(GROUPED_QUERY_HEADS):
+                q[b, h] = syn.head_stream(900 + G, b, h, syn.TENSOR_Q, (n_dec, DK), "bf16")
+        k = np.empty((B, Hkv, N + n_dec, DK), np.float32)
+        v = np.empty((B, Hkv, N + n_dec, DV), np.float32)
+        for b in range(B):
+            for h in range(Hkv):
+                k[b, h] = syn.head_stream(900 + G, b, h, syn.TENSOR_K, (N + n_dec, DK), "bf16")
+                v[b, h] = syn.head_stream(900 + G, b, h, syn.TENSOR_V, (N + n_dec, DV), "bf16")
+        up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(torch.bfloat16)
+        kk, vv = up(k[:, :, :N]), up(v[:, :, :N])
+        _, S0 = sata.prefill(kk, kk, vv, P, CHUNK)  # the state does not depend on q
+        dq, dk_, dv_ = (up(a.transpose(2, 0, 1, 3)) for a in (q, k[:, :, N:], v[:, :, N:]))
+        del q, k, v, kk, vv
+        S = torch.empty_like(S0)
+        ydec = torch.empty(n_dec, B, GROUPED_QUERY_HEADS, DV, dtype=torch.bfloat16, device="cuda")
+
+        def steps_once():
+            for t in range(n_dec):
+                sata.decode_step_grouped(S, dq[t], dk_[t], dv_[t], P, y=ydec[t])
+        ms = []
+        for it in range(args.warmup + args.steps):
+            S.copy_(S0)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            steps_once()
+            e1.record()
+            torch.cuda.synchronize()
+            if it >= args.warmup:
+                ms.append(e0.elapsed_time(e1))
+        step_ms = sum(ms) / len(ms) / n_dec
+        t_total += step_ms * n_dec
+        D = feature_count(DK, P)
+        dbytes = B * Hkv * (8 * D * (DV + 1) + 2 * (DK + DV)) + B * GROUPED_QUERY_HEADS * 2 * (DK + DV)
+        ach = dbytes / (step_ms * 1e-3) / 1e9
+        r = {"kernel": "decode_grouped_kernel (one launch per step)", "bound": "hbm", "achieved": ach,
+             "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": ach / PEAK_HBM_GBS, "traffic": None,
+             "work_per_launch": dbytes}
+        per_G[str(G)] = {"kv_heads": B * Hkv, "query_heads": B * GROUPED_QUERY_HEADS, "decode_us_per_step": step_ms * 1e3,
+                         "decode_tokens_per_s": B / (step_ms * 1e-3),
+                         "query_head_tokens_per_s": B * GROUPED_QUERY_HEADS / (step_ms * 1e-3), "roofline": r}
+        roof = r if roof is None else roof
+        print(f"grouped G={G}: {step_ms * 1e3:.1f} us/step, {ach:.0f} GB/s", file=sys.stderr, flush=True)
+        del S, S0, dq, dk_, dv_, ydec
+        torch.cuda.empty_cache()
+    line = {
+        "metric": "prefill tokens/s + decode tokens/s (d_k=32,P=4); % MFMA/HBM roofline",
+        "value": B * n_dec * len(GROUPED_GS) / (t_total * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": t_total, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": (f"decode_grouped: B={B}, {GROUPED_QUERY_HEADS} query heads, d_k=d_v={DK}, P={P}, bf16, "
+                                f"{N}-token prefill of the key/value heads then {n_dec} grouped decode steps, "
+                                f"G={'/'.join(map(str, GROUPED_GS))}"),
+                   "global_batch": B, "seq_len": N, "decode_steps": n_dec, "heads": GROUPED_QUERY_HEADS,
+                   "d_k": DK, "d_v": DV, "P": P, "parallelism": "single GPU"},
+        "per_G": per_G,
+        "roofline": roof,
+    }
+    return line
+
+
 CONTEXT_SWEEP = [(8, 8), (16, 8), (32, 8), (64, 7)]  # (d, largest power of ten of the context)
 CONTEXT_DECODE = 64
 
@@ -549,6 +634,9 @@ def main():
     import paper_2602_00294_amd as sata
     sata.load_library()
     assert torch.cuda.is_available(), "no GPU"
+    if args.workload == "decode_grouped":
+        print(json.dumps(run_decode_grouped(args, sata, torch)), flush=True)
+        return
     if args.workload == "context_sweep":
         print(json.dumps(run_context_sweep(args, sata, torch)), flush=True)
         return

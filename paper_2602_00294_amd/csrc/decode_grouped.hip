@@ -123,8 +123,27 @@ decode_grouped_kernel(float* __restrict__ S, const T* __restrict__ q, const T* _
     cur[u] = Sv[(active && g < nv && m_lo + u < m_hi) ? g : 0];
   }
   lx = lead ? lx : 0.0f;
-  __syncthreads();
-  for (int64_t f = row_lo + tid; f <= row_hi; f += NTH) {
+  // the first two table entries of this thread's rows load while the
+  // coordinates reach LDS (the barrier waits for LDS only)
+  uint64_t pk0[2];
+  float w0[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int64_t f = row_lo + tid + (int64_t)NTH * u;
+    pk0[u] = (f <= row_hi) ? packed[f] : 0;
+    w0[u] = (f <= row_hi) ? weight[f] : 0.0f;
+  }
+  lds_wait_barrier();
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int64_t r = tid + (int64_t)NTH * u;
+    if (row_lo + r <= row_hi) {
+      fk[r] = feature_value(pk0[u], w0[u], xk);
+#pragma unroll
+      for (int g = 0; g < G; ++g) fq[r * G + g] = feature_value(pk0[u], w0[u], xq + g * dk);
+    }
+  }
+  for (int64_t f = row_lo + tid + 2 * (int64_t)NTH; f <= row_hi; f += NTH) {
     const uint64_t pk = packed[f];
     const float w = weight[f];
     const int64_t r = f - row_lo;
@@ -229,10 +248,20 @@ decode_grouped_kernel(float* __restrict__ S, const T* __restrict__ q, const T* _
     __syncthreads();
     if (arrived[0] != npieces - 1) return;  // a later piece finishes the head
     for (int i = tid; i < GE; i += NTH) {
+      // the other pieces' sums, 8 loads in flight at a time, added in piece order
       const float* const xp = xpart + bh * npieces * GE + i;
       float a = 0.0f;
-      for (int p = 0; p < npieces; ++p)
-        a += (p == piece) ? o[i] : __hip_atomic_load(xp + (int64_t)p * GE, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      for (int p0 = 0; p0 < npieces; p0 += 8) {
+        float w[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          w[u] = (p0 + u < npieces && p0 + u != piece)
+                     ? __hip_atomic_load(xp + (int64_t)(p0 + u) * GE, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                     : 0.0f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (p0 + u < npieces) a += (p0 + u == piece) ? o[i] : w[u];
+      }
       o[i] = a;
     }
     if (tid == 0) __hip_atomic_store(cnt + bh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
