@@ -56,11 +56,11 @@ struct GroupRow<8> {
 };
 
 // LDS layout (floats): fk [rows4] | fq [rows4][G] | xq [G][dk] | xk [dk] |
-// ve [E] | red [4 tu] | part [8][E] | o [G][E] | lo_val [G][8] | lo_col [8]
+// ve [E] | red [2][4 tu] | part [2][8][E] | o [G][E] | lo_val [G][8] | lo_col [8]
 // with rows4 = max_rows rounded up to a multiple of 4 (fq 16-byte aligned).
 __host__ __device__ inline size_t grouped_lds_floats(int max_rows, int G, int dk, int E, int tu) {
   const size_t rows4 = ((size_t)max_rows + 3) & ~(size_t)3;
-  return rows4 * (1 + G) + (size_t)G * dk + dk + E + 4 * (size_t)tu + 8 * (size_t)E + (size_t)G * E + 8 * (size_t)G +
+  return rows4 * (1 + G) + (size_t)G * dk + dk + E + 8 * (size_t)tu + 16 * (size_t)E + (size_t)G * E + 8 * (size_t)G +
          8;
 }
 
@@ -90,9 +90,9 @@ decode_grouped_kernel(float* __restrict__ S, const T* __restrict__ q, const T* _
   float* const xq = fq + (size_t)rows4 * G;
   float* const xk = xq + G * dk;
   float* const ve = xk + dk;
-  float* const red = ve + E;
-  float* const part = red + 4 * tu;
-  float* const o = part + 8 * E;
+  float* const red = ve + E;       // [2][4 tu]
+  float* const part = red + 8 * tu;  // [2][8][E]
+  float* const o = part + 16 * E;
   float* const lo_val = o + G * E;
   int* const lo_col = (int*)(lo_val + 8 * G);
 
@@ -209,30 +209,34 @@ decode_grouped_kernel(float* __restrict__ S, const T* __restrict__ q, const T* _
       if (!more) break;
     }
   }
-  // column sums, one query head at a time through the same LDS rows
+  // column sums, one query head per round through two alternating sets of
+  // LDS rows, so that a round needs one barrier: round g stores head g's
+  // per-thread sums, then (after the barrier) adds them into 8 partial rows
+  // per column and adds up head g-1's partial rows
+  const int j8 = tid % E, pp8 = tid / E;
+  const int p0 = ((j8 - a0) % E + E) % E;  // red[p] holds column (a0 + p) mod E
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-    if (active) {
+  for (int g = 0; g <= G; ++g) {
+    float* const rb = red + (g & 1) * 4 * tu;
+    if (g < G && active) {
 #pragma unroll
-      for (int c = 0; c < 4; ++c) red[4 * tid + c] = acc[g][c];
+      for (int c = 0; c < 4; ++c) rb[4 * tid + c] = acc[g < G ? g : 0][c];
     }
     __syncthreads();
-    if (tid < 8 * E) {
-      const int j = tid % E, pp = tid / E;
-      const int p0 = ((j - a0) % E + E) % E;  // red[p] holds column (a0 + p) mod E
+    if (g < G && tid < 8 * E) {
       float a = 0.0f;
-      for (int p = p0 + E * pp; p < 4 * tu; p += 8 * E) a += red[p];
-      part[tid] = a;
+      for (int p = p0 + E * pp8; p < 4 * tu; p += 8 * E) a += rb[p];
+      part[(g & 1) * 8 * E + tid] = a;
     }
-    __syncthreads();
-    if (tid < E) {
+    if (g > 0 && tid < E) {
+      const float* const pb = part + ((g - 1) & 1) * 8 * E;
       float a = 0.0f;
 #pragma unroll
-      for (int pp = 0; pp < 8; ++pp) a += part[pp * E + tid];
-      o[g * E + tid] = a;
+      for (int pp = 0; pp < 8; ++pp) a += pb[pp * E + tid];
+      o[(g - 1) * E + tid] = a;
     }
-    __syncthreads();
   }
+  __syncthreads();
   if (tid < G) {
     for (int i = 0; i < nleft; ++i) o[tid * E + lo_col[i]] += lo_val[tid * 8 + i];  // leftovers, in element order
   }
