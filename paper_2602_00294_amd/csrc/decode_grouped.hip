@@ -225,6 +225,7 @@ decode_grouped_kernel(float* __restrict__ S, const T* __restrict__ q, const T* _
     __syncthreads();
     if (g < G && tid < 8 * E) {
       float a = 0.0f;
+#pragma unroll 8
       for (int p = p0 + E * pp8; p < 4 * tu; p += 8 * E) a += rb[p];
       part[(g & 1) * 8 * E + tid] = a;
     }
