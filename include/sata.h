@@ -26,7 +26,12 @@
  *    memory on the current HIP device.  Activations (q, k, v, y) use the layout
  *    [B][H][n][d] (prefill) or [B][H][d] (decode).  Outputs must not alias inputs.
  *  - `stream` is a hipStream_t (NULL = the default stream).  Calls are
- *    asynchronous on that stream and never synchronise the host.
+ *    asynchronous on that stream.  The host waits for the stream in two cases
+ *    only: the first call on a device that needs a given (d_k, P) feature
+ *    table (it uploads the table and waits for the copy, since every stream of
+ *    the device shares it), and a call whose workspace on that stream must grow
+ *    (it waits before freeing the smaller one).  A caller that captures calls
+ *    into a graph makes one call of each shape first, outside the capture.
  *  - Arguments are validated on the host before anything is launched; on any
  *    error return nothing has been written and sata_last_error() explains it.
  *  - The library owns only per-device caches (feature tables, workspaces),
@@ -99,6 +104,15 @@ sata_status sata_feature_map(const void* x, sata_dtype xt, int64_t rows, int d, 
 sata_status sata_prefill(const void* q, const void* k, const void* v, sata_dtype dt,
                          int B, int H, int n, int d_k, int d_v, int P, int chunk,
                          void* y, float* S_out, void* stream);
+
+/* Precision of the operands of the state contractions that sata_prefill uses
+ * for these arguments (host only, no GPU use; same validation as sata_prefill):
+ * *operands = SATA_BF16 when they run on the matrix cores with bfloat16
+ * operands and float32 accumulation, SATA_F32 when every product is formed in
+ * float32.  The state is float32 in both cases; callers use this to know the
+ * accuracy to expect (about 2^-8 relative per term with bfloat16 operands). */
+sata_status sata_prefill_operands(sata_dtype dt, int B, int H, int n, int d_k, int d_v, int P, int chunk,
+                                  sata_dtype* operands);
 
 /* One decode step for every (b, h) (App. A2, the linear recurrences for Z_{p,T}
  * and S_{p,T}, then the readout at q_T): S += phi(k) (x) [v, 1], then

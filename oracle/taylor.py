@@ -34,6 +34,10 @@ What is computed (sections of the paper in brackets):
                         and their readout, as the paper's linear-attention
                         recurrence [App. A2, accumulated feature states and
                         evaluation at the query].
+* ``state_abs_ref``     the same sum over absolute values, sum_t |phi(k_t)| (x)
+                        |[v_t, 1]|: the size of the terms that make up each
+                        state entry, against which a rounded state is judged
+                        [App. A2, accumulated feature states].
 * ``feature_count`` / ``state_elems`` / ``flops_per_token``
                         the closed forms of Sec. 2.6 and Sec. 2.7.
 
@@ -66,7 +70,7 @@ import numpy as np
 __all__ = [
     "taylor_poly", "taylor_attention", "taylor_attention_rows", "softmax_attention",
     "softmax_attention_rows", "multi_indices", "multiplicity", "alpha", "feature_weights",
-    "phi_ref", "state_ref", "readout_ref", "recurrent_attention", "decode_ref",
+    "phi_ref", "state_ref", "state_abs_ref", "readout_ref", "recurrent_attention", "decode_ref",
     "feature_count", "degree_count", "state_elems", "flops_per_token",
 ]
 
@@ -283,6 +287,17 @@ def state_ref(k, v, P: int) -> np.ndarray:
     """S = sum_t phi(k_t) (x) [v_t, 1]  ->  [D, d_v + 1] (the Z_{p,T} and S_{p,T}
     of every degree stacked, normaliser in the last column)."""
     return phi_ref(k, P).T @ _extend(_as64(v))
+
+
+def state_abs_ref(k, v, P: int) -> np.ndarray:
+    """sum_t |phi(k_t)| (x) |[v_t, 1]|  ->  [D, d_v + 1].
+
+    Entry (f, j) is the sum of the magnitudes of the terms whose sum is the
+    state entry S[f, j].  A state accumulated in a precision with unit
+    roundoff u (per term, plus the rounding of the running sums) is off by at
+    most a small multiple of u times this entry, whatever the cancellation
+    inside the sum; a misplaced row or column is off by the entry itself."""
+    return np.abs(phi_ref(k, P)).T @ np.abs(_extend(_as64(v)))
 
 
 def readout_ref(S, q, P: int) -> np.ndarray:

@@ -48,6 +48,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.sata_feature_map.restype = i32
     lib.sata_prefill.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp]
     lib.sata_prefill.restype = i32
+    lib.sata_prefill_operands.argtypes = [i32, i32, i32, i32, i32, i32, i32, i32, ctypes.POINTER(i32)]
+    lib.sata_prefill_operands.restype = i32
     lib.sata_decode_step.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp]
     lib.sata_decode_step.restype = i32
     lib.sata_decode_step_grouped.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp, vp]
@@ -108,11 +110,30 @@ def _dtype_code(t) -> int:
     raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
 
 
-def _check_tensor(t, name: str):
+def _check_tensor(t, name: str, device=None):
     if not t.is_cuda:
         raise ValueError(f"{name} must be a GPU tensor")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
+
+
+def _check_same_dtype(ref, **tensors):
+    for name, t in tensors.items():
+        if t.dtype != ref.dtype:
+            raise TypeError(f"{name} is {t.dtype}, expected {ref.dtype} like q")
+
+
+def _check_shape(t, name: str, shape):
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+
+def _check_state(S, shape):
+    if S.dtype != _torch().float32:
+        raise TypeError("S must be float32")
+    _check_shape(S, "S", shape)
 
 
 def _stream_ptr():
@@ -123,72 +144,106 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None and t.numel() > 0 else ctypes.c_void_p(None)
 
 
+def _features(d: int, P: int) -> int:
+    D = feature_count(d, P)
+    if D < 0:
+        raise ValueError(f"invalid d={d} or P={P}")
+    return D
+
+
 def feature_map(x, P: int):
     """phi(x) for x [..., d] (float32 or bfloat16) -> float32 [..., D]."""
     torch = _torch()
-    _check_tensor(x, "x")
+    code = _dtype_code(x)
     d = x.shape[-1]
     rows = x.numel() // d if d else 0
-    D = feature_count(d, P)
-    if D < 0:
-        raise ValueError("invalid d or P")
+    D = _features(d, P)
+    _check_tensor(x, "x")
     phi = torch.empty(*x.shape[:-1], D, dtype=torch.float32, device=x.device)
-    _check(load_library().sata_feature_map(_ptr(x), _dtype_code(x), rows, d, P, _ptr(phi), _stream_ptr()),
-           "sata_feature_map")
+    with torch.cuda.device(x.device):
+        _check(load_library().sata_feature_map(_ptr(x), code, rows, d, P, _ptr(phi), _stream_ptr()),
+               "sata_feature_map")
     return phi
+
+
+def prefill_operands(dtype, B: int, H: int, n: int, d_k: int, d_v: int, P: int, chunk: int = 64) -> str:
+    """Operand precision ('bf16' or 'f32') of the state contractions that
+    prefill uses for these arguments (host only)."""
+    torch = _torch()
+    code = {torch.float32: SATA_F32, torch.bfloat16: SATA_BF16}.get(dtype)
+    if code is None:
+        raise TypeError(f"unsupported dtype {dtype}; use float32 or bfloat16")
+    out = ctypes.c_int(-1)
+    _check(load_library().sata_prefill_operands(code, B, H, n, d_k, d_v, P, chunk, ctypes.byref(out)),
+           "sata_prefill_operands")
+    return "bf16" if out.value == SATA_BF16 else "f32"
 
 
 def prefill(q, k, v, P: int, chunk: int = 64, want_state: bool = True, y=None, S=None):
     """Causal prefill.  q, k: [B, H, n, d_k]; v: [B, H, n, d_v].
 
     Returns (y [B, H, n, d_v] in the input dtype, S [B, H, D, d_v+1] float32 or None).
-    Preallocated outputs may be passed as y= and S=.
+    Preallocated outputs may be passed as y= and S=.  Shapes and dtypes are
+    checked before anything is launched.
     """
     torch = _torch()
-    for name, t in (("q", q), ("k", k), ("v", v)):
-        _check_tensor(t, name)
-    if q.dtype != k.dtype or q.dtype != v.dtype:
-        raise TypeError("q, k, v must share one dtype")
+    code = _dtype_code(q)
+    _check_same_dtype(q, k=k, v=v)
+    if q.dim() != 4 or v.dim() != 4:
+        raise ValueError("q, k, v must be [B, H, n, d]")
     B, H, n, dk = q.shape
     dv = v.shape[-1]
-    if tuple(k.shape) != (B, H, n, dk) or tuple(v.shape[:3]) != (B, H, n):
-        raise ValueError("q, k, v shapes disagree")
-    D = feature_count(dk, P)
+    _check_shape(k, "k", (B, H, n, dk))
+    _check_shape(v, "v", (B, H, n, dv))
+    D = _features(dk, P)
+    if y is not None:
+        _check_same_dtype(q, y=y)
+        _check_shape(y, "y", (B, H, n, dv))
+    if S is not None:
+        _check_state(S, (B, H, D, dv + 1))
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check_tensor(t, name, q.device)
     if y is None:
         y = torch.empty(B, H, n, dv, dtype=q.dtype, device=q.device)
     if want_state and S is None:
         S = torch.empty(B, H, D, dv + 1, dtype=torch.float32, device=q.device)
+    _check_tensor(y, "y", q.device)
     if S is not None:
-        _check_tensor(S, "S")
-        if S.dtype != torch.float32 or tuple(S.shape) != (B, H, D, dv + 1):
-            raise ValueError("S must be float32 [B, H, D, d_v+1]")
-    _check_tensor(y, "y")
-    _check(load_library().sata_prefill(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, H, n, dk, dv, P, chunk,
-                                       _ptr(y), _ptr(S) if S is not None else ctypes.c_void_p(None),
-                                       _stream_ptr()), "sata_prefill")
+        _check_tensor(S, "S", q.device)
+    with torch.cuda.device(q.device):
+        _check(load_library().sata_prefill(_ptr(q), _ptr(k), _ptr(v), code, B, H, n, dk, dv, P, chunk,
+                                           _ptr(y), _ptr(S) if S is not None else ctypes.c_void_p(None),
+                                           _stream_ptr()), "sata_prefill")
     return y, S
 
 
 def decode_step(S, q, k, v, P: int, y=None):
     """One decode step in place on S [B, H, D, d_v+1]; q, k: [B, H, d_k]; v: [B, H, d_v].
 
-    Returns y [B, H, d_v] in the input dtype.
+    Returns y [B, H, d_v] in the input dtype.  Shapes and dtypes are checked
+    before anything is launched.
     """
     torch = _torch()
-    for name, t in (("S", S), ("q", q), ("k", k), ("v", v)):
-        _check_tensor(t, name)
-    if S.dtype != torch.float32:
-        raise TypeError("S must be float32")
+    code = _dtype_code(q)
+    _check_same_dtype(q, k=k, v=v)
+    if q.dim() != 3 or v.dim() != 3:
+        raise ValueError("q, k, v must be [B, H, d]")
     B, H, dk = q.shape
     dv = v.shape[-1]
-    D = feature_count(dk, P)
-    if tuple(S.shape) != (B, H, D, dv + 1):
-        raise ValueError(f"S must be [B, H, {D}, {dv + 1}]")
+    _check_shape(k, "k", (B, H, dk))
+    _check_shape(v, "v", (B, H, dv))
+    _check_state(S, (B, H, _features(dk, P), dv + 1))
+    if y is not None:
+        _check_same_dtype(q, y=y)
+        _check_shape(y, "y", (B, H, dv))
+    for name, t in (("S", S), ("q", q), ("k", k), ("v", v)):
+        _check_tensor(t, name, q.device)
     if y is None:
         y = torch.empty(B, H, dv, dtype=q.dtype, device=q.device)
-    _check_tensor(y, "y")
-    _check(load_library().sata_decode_step(_ptr(S), _ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, H, dk, dv, P,
-                                           _ptr(y), _stream_ptr()), "sata_decode_step")
+    _check_tensor(y, "y", q.device)
+    with torch.cuda.device(q.device):
+        _check(load_library().sata_decode_step(_ptr(S), _ptr(q), _ptr(k), _ptr(v), code, B, H, dk, dv, P,
+                                               _ptr(y), _stream_ptr()), "sata_decode_step")
     return y
 
 
@@ -199,24 +254,31 @@ def decode_step_grouped(S, q, k, v, P: int, y=None):
     head h); k: [B, H_kv, d_k]; v: [B, H_kv, d_v].  Returns y [B, H_q, d_v].
     """
     torch = _torch()
-    for name, t in (("S", S), ("q", q), ("k", k), ("v", v)):
-        _check_tensor(t, name)
-    if S.dtype != torch.float32:
-        raise TypeError("S must be float32")
+    code = _dtype_code(q)
+    _check_same_dtype(q, k=k, v=v)
+    if q.dim() != 3 or k.dim() != 3 or v.dim() != 3:
+        raise ValueError("q [B, G*H_kv, d_k], k [B, H_kv, d_k], v [B, H_kv, d_v] expected")
     B, Hq, dk = q.shape
     Hkv = k.shape[1]
     dv = v.shape[-1]
-    if tuple(k.shape) != (B, Hkv, dk) or tuple(v.shape[:2]) != (B, Hkv) or Hq % Hkv:
-        raise ValueError("q [B, G*H_kv, d_k], k [B, H_kv, d_k], v [B, H_kv, d_v] expected")
+    if Hkv < 1 or Hq % Hkv:
+        raise ValueError("the query head count must be a multiple of the key/value head count")
+    _check_shape(k, "k", (B, Hkv, dk))
+    _check_shape(v, "v", (B, Hkv, dv))
     G = Hq // Hkv
-    D = feature_count(dk, P)
-    if tuple(S.shape) != (B, Hkv, D, dv + 1):
-        raise ValueError(f"S must be [B, H_kv, {D}, {dv + 1}]")
+    _check_state(S, (B, Hkv, _features(dk, P), dv + 1))
+    if y is not None:
+        _check_same_dtype(q, y=y)
+        _check_shape(y, "y", (B, Hq, dv))
+    for name, t in (("S", S), ("q", q), ("k", k), ("v", v)):
+        _check_tensor(t, name, q.device)
     if y is None:
         y = torch.empty(B, Hq, dv, dtype=q.dtype, device=q.device)
-    _check_tensor(y, "y")
-    _check(load_library().sata_decode_step_grouped(_ptr(S), _ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, Hkv, G,
-                                                   dk, dv, P, _ptr(y), _stream_ptr()), "sata_decode_step_grouped")
+    _check_tensor(y, "y", q.device)
+    with torch.cuda.device(q.device):
+        _check(load_library().sata_decode_step_grouped(_ptr(S), _ptr(q), _ptr(k), _ptr(v), code, B, Hkv, G,
+                                                       dk, dv, P, _ptr(y), _stream_ptr()),
+               "sata_decode_step_grouped")
     return y
 
 

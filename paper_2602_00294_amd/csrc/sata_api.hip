@@ -170,6 +170,29 @@ sata_status check_dims(int d_k, int d_v, int P, int64_t* D) {
   return SATA_OK;
 }
 
+sata_status check_prefill_args(sata_dtype dt, int B, int H, int n, int d_k, int d_v, int P, int chunk,
+                               int64_t* D) {
+  if (!valid_dtype(dt)) return fail(SATA_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
+  if (B < 1 || H < 1) return fail(SATA_ERR_INVALID_ARG, "B=%d H=%d must be >= 1", B, H);
+  if (n < 0) return fail(SATA_ERR_INVALID_ARG, "n=%d < 0", n);
+  sata_status st = check_dims(d_k, d_v, P, D);
+  if (st != SATA_OK) return st;
+  if (chunk != 16 && chunk != 32 && chunk != 64 && chunk != 128)
+    return fail(SATA_ERR_UNSUPPORTED, "chunk=%d; supported: 16, 32, 64, 128", chunk);
+  if ((int64_t)B * H > kMaxHeads) return fail(SATA_ERR_TOO_LARGE, "B*H=%lld exceeds %d", (long long)B * H, kMaxHeads);
+  return SATA_OK;
+}
+
+enum class PrefillPath { kMfma32, kBlocks, kFloat32 };
+
+// The kernel family that serves a validated prefill request.
+PrefillPath prefill_path(sata_dtype dt, int BH, int n, int d_k, int d_v, int P, int chunk) {
+  sata::MfmaPrefillPlan mp;
+  if (dt == SATA_BF16 && sata::plan_prefill_mfma(BH, n, d_k, d_v, P, chunk, &mp)) return PrefillPath::kMfma32;
+  if (dt == SATA_BF16 && sata::plan_prefill_blocks(BH, n, d_k, d_v, P, chunk, &mp)) return PrefillPath::kBlocks;
+  return PrefillPath::kFloat32;
+}
+
 }  // namespace
 
 extern "C" {
@@ -233,17 +256,21 @@ sata_status sata_feature_map(const void* x, sata_dtype xt, int64_t rows, int d, 
   return ok();
 }
 
+sata_status sata_prefill_operands(sata_dtype dt, int B, int H, int n, int d_k, int d_v, int P, int chunk,
+                                  sata_dtype* operands) {
+  if (!operands) return fail(SATA_ERR_INVALID_ARG, "null output pointer");
+  int64_t D = 0;
+  sata_status st = check_prefill_args(dt, B, H, n, d_k, d_v, P, chunk, &D);
+  if (st != SATA_OK) return st;
+  *operands = prefill_path(dt, B * H, n, d_k, d_v, P, chunk) == PrefillPath::kFloat32 ? SATA_F32 : SATA_BF16;
+  return ok();
+}
+
 sata_status sata_prefill(const void* q, const void* k, const void* v, sata_dtype dt, int B, int H, int n,
                          int d_k, int d_v, int P, int chunk, void* y, float* S_out, void* stream) {
-  if (!valid_dtype(dt)) return fail(SATA_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
-  if (B < 1 || H < 1) return fail(SATA_ERR_INVALID_ARG, "B=%d H=%d must be >= 1", B, H);
-  if (n < 0) return fail(SATA_ERR_INVALID_ARG, "n=%d < 0", n);
   int64_t D = 0;
-  sata_status st = check_dims(d_k, d_v, P, &D);
+  sata_status st = check_prefill_args(dt, B, H, n, d_k, d_v, P, chunk, &D);
   if (st != SATA_OK) return st;
-  if (chunk != 16 && chunk != 32 && chunk != 64 && chunk != 128)
-    return fail(SATA_ERR_UNSUPPORTED, "chunk=%d; supported: 16, 32, 64, 128", chunk);
-  if ((int64_t)B * H > kMaxHeads) return fail(SATA_ERR_TOO_LARGE, "B*H=%lld exceeds %d", (long long)B * H, kMaxHeads);
   if (n > 0 && (!q || !k || !v || !y)) return fail(SATA_ERR_INVALID_ARG, "null tensor pointer");
   const int BH = B * H;
   const int E = d_v + 1;
@@ -261,14 +288,15 @@ sata_status sata_prefill(const void* q, const void* k, const void* v, sata_dtype
 
   // bf16 fast path on the matrix cores where a tuned kernel exists
   sata::MfmaPrefillPlan mp;
-  if (dt == SATA_BF16 && sata::plan_prefill_mfma(BH, n, d_k, d_v, P, chunk, &mp)) {
+  const PrefillPath path = prefill_path(dt, BH, n, d_k, d_v, P, chunk);
+  if (path == PrefillPath::kMfma32 && sata::plan_prefill_mfma(BH, n, d_k, d_v, P, chunk, &mp)) {
     void* ws = nullptr;
     if ((st = get_workspace(mp.workspace_bytes, s, &ws)) != SATA_OK) return st;
     e = sata::launch_prefill_mfma(q, k, v, y, S_out, BH, n, d_k, d_v, P, chunk, mp, ws, s);
     if (e != hipSuccess) return hip_fail(e, "prefill (matrix-core) launch");
     return ok();
   }
-  if (dt == SATA_BF16 && sata::plan_prefill_blocks(BH, n, d_k, d_v, P, chunk, &mp)) {
+  if (path == PrefillPath::kBlocks && sata::plan_prefill_blocks(BH, n, d_k, d_v, P, chunk, &mp)) {
     void* ws = nullptr;
     if ((st = get_workspace(mp.workspace_bytes, s, &ws)) != SATA_OK) return st;
     e = sata::launch_prefill_blocks(q, k, v, y, S_out, BH, n, d_k, d_v, P, chunk, mp, ws, s);

@@ -110,3 +110,88 @@ def test_decode_and_feature_map_validation(lib):
 def test_status_strings(lib):
     for code in (0, -1, -2, -3, -4):
         assert lib.sata_status_string(code)
+
+
+def test_prefill_operands_query(lib):
+    out = ctypes.c_int(-1)
+    # float32 inputs always take float32 products; the benchmark's bf16 shape takes the matrix cores
+    assert lib.sata_prefill_operands(0, 8, 32, 8192, 32, 32, 4, 64, ctypes.byref(out)) == 0 and out.value == 0
+    assert lib.sata_prefill_operands(1, 8, 32, 8192, 32, 32, 4, 64, ctypes.byref(out)) == 0 and out.value == 1
+    # the same validation as the prefill itself
+    assert lib.sata_prefill_operands(1, 1, 1, 8, 32, 32, 4, 48, ctypes.byref(out)) == -2
+    assert lib.sata_prefill_operands(7, 1, 1, 8, 32, 32, 4, 64, ctypes.byref(out)) == -1
+    assert lib.sata_prefill_operands(1, 1, 1, 8, 32, 32, 4, 64, None) == -1
+    torch = pytest.importorskip("torch")
+    assert bnd.prefill_operands(torch.float32, 1, 1, 100, 8, 8, 4, 64) == "f32"
+
+
+class TestBindingRejectsBeforeLaunch:
+    """The tensor wrappers check dtypes and shapes before anything reaches the
+    library, so a mismatched output or input is refused instead of being
+    written or read past its end.  (CPU tensors: the checks come before the
+    device check.)"""
+
+    @pytest.fixture(autouse=True)
+    def _torch(self):
+        self.torch = pytest.importorskip("torch")
+
+    def t(self, *shape, dtype=None):
+        return self.torch.zeros(*shape, dtype=dtype or self.torch.float32)
+
+    def test_prefill(self):
+        bf = self.torch.bfloat16
+        q, k, v = self.t(1, 2, 8, 4), self.t(1, 2, 8, 4), self.t(1, 2, 8, 3)
+        with pytest.raises(TypeError):
+            bnd.prefill(q, k.to(bf), v, 3)
+        with pytest.raises(TypeError):
+            bnd.prefill(q, k, v.to(bf), 3)
+        with pytest.raises(ValueError):
+            bnd.prefill(q, self.t(1, 2, 7, 4), v, 3)          # short k
+        with pytest.raises(ValueError):
+            bnd.prefill(q, k, self.t(1, 2, 7, 3), 3)          # short v
+        with pytest.raises(TypeError):
+            bnd.prefill(q, k, v, 3, y=self.t(1, 2, 8, 3, dtype=bf))
+        with pytest.raises(ValueError):
+            bnd.prefill(q, k, v, 3, y=self.t(1, 2, 8, 2))
+        with pytest.raises(ValueError):
+            bnd.prefill(q, k, v, 3, S=self.t(1, 2, 14, 4))     # D = 15 at d=4, P=3
+        with pytest.raises(TypeError):
+            bnd.prefill(q, k, v, 3, S=self.t(1, 2, 15, 4, dtype=bf))
+        with pytest.raises(ValueError, match="GPU"):
+            bnd.prefill(q, k, v, 3)                           # consistent, but not on a GPU
+
+    def test_decode(self):
+        bf = self.torch.bfloat16
+        S, q, k, v = self.t(2, 3, 15, 6), self.t(2, 3, 4), self.t(2, 3, 4), self.t(2, 3, 5)
+        with pytest.raises(TypeError):
+            bnd.decode_step(S, q, k.to(bf), v, 3)
+        with pytest.raises(TypeError):
+            bnd.decode_step(S, q, k, v.to(bf), 3)
+        with pytest.raises(ValueError):
+            bnd.decode_step(S, q, self.t(2, 3, 3), v, 3)      # k of the wrong width
+        with pytest.raises(ValueError):
+            bnd.decode_step(S, q, k, self.t(2, 2, 5), 3)      # v of too few heads
+        with pytest.raises(TypeError):
+            bnd.decode_step(S, q, k, v, 3, y=self.t(2, 3, 5, dtype=bf))
+        with pytest.raises(ValueError):
+            bnd.decode_step(S, q, k, v, 3, y=self.t(2, 3, 4))
+        with pytest.raises(ValueError):
+            bnd.decode_step(self.t(2, 3, 15, 5), q, k, v, 3)
+        with pytest.raises(ValueError, match="GPU"):
+            bnd.decode_step(S, q, k, v, 3)
+
+    def test_decode_grouped(self):
+        bf = self.torch.bfloat16
+        S, q, k, v = self.t(1, 2, 15, 6), self.t(1, 8, 4), self.t(1, 2, 4), self.t(1, 2, 5)
+        with pytest.raises(TypeError):
+            bnd.decode_step_grouped(S, q, k.to(bf), v, 3)
+        with pytest.raises(ValueError):
+            bnd.decode_step_grouped(S, self.t(1, 7, 4), k, v, 3)   # 7 query heads over 2 key/value heads
+        with pytest.raises(ValueError):
+            bnd.decode_step_grouped(S, q, k, self.t(1, 3, 5), 3)
+        with pytest.raises(TypeError):
+            bnd.decode_step_grouped(S, q, k, v, 3, y=self.t(1, 8, 5, dtype=bf))
+        with pytest.raises(ValueError):
+            bnd.decode_step_grouped(S, q, k, v, 3, y=self.t(1, 2, 5))
+        with pytest.raises(ValueError, match="GPU"):
+            bnd.decode_step_grouped(S, q, k, v, 3)

@@ -10,8 +10,7 @@ import pytest
 
 import oracle
 import sata_synth as syn
-from gpu_util import TOL, to_dev, to_host
-from oracle.metrics import max_row_rel_error, state_rel_error
+from gpu_util import check_rows, check_state, operands, to_dev, to_host, y_tol
 
 pytestmark = pytest.mark.gpu
 
@@ -58,6 +57,7 @@ def test_grouped_decode_matches_oracle(sata, B, Hkv, G, n1, n2, d, P, dtype):
     _say(f"grouped decode B={B} H_kv={Hkv} G={G} n1={n1} n2={n2} d={d} P={P} {dtype}")
     q, k, v = _inputs(80 + d, B, Hkv, G, n1 + n2, d, dtype)
     S = _state_after_prefill(sata, k, v, n1, P, dtype)
+    ops = operands(sata, dtype, B, Hkv, n1, d, d, P, 32) if n1 > 0 else "f32"
     ys = []
     for t in range(n1, n1 + n2):
         ys.append(to_host(sata.decode_step_grouped(S, to_dev(q[:, :, t].copy(), dtype), to_dev(k[:, :, t].copy(), dtype),
@@ -69,11 +69,9 @@ def test_grouped_decode_matches_oracle(sata, B, Hkv, G, n1, n2, d, P, dtype):
             h = hq // G
             yr, _, kap = oracle.taylor_attention_rows(q[b, hq], k[b, h], v[b, h], P, list(range(n1, n1 + n2)))
             got = np.stack([yy[b, hq] for yy in ys])
-            err, _ = max_row_rel_error(got, yr, kap)
-            assert err <= TOL[dtype], f"b{b} query head {hq}: {err:.3e}"
+            check_rows(got, yr, kap, y_tol(ops, dtype), P, f"b{b} query head {hq}")
         for h in range(Hkv):
-            s_err = state_rel_error(S_host[b, h], oracle.state_ref(k[b, h], v[b, h], P))
-            assert s_err <= TOL[dtype], f"state b{b} h{h}: {s_err:.3e}"
+            check_state(S_host[b, h], k[b, h], v[b, h], P, ops, n1, 32, f"state b{b} h{h}", steps=n2)
 
 
 def test_grouped_decode_deterministic_and_g1_is_decode_step(sata):

@@ -9,8 +9,7 @@ import pytest
 
 import oracle
 import sata_synth as syn
-from gpu_util import TOL, check_prefill_head, to_dev, to_host
-from oracle.metrics import max_row_rel_error, state_rel_error
+from gpu_util import check_prefill_head, check_rows, check_state, operands, to_dev, to_host, y_tol
 
 pytestmark = pytest.mark.gpu
 
@@ -34,11 +33,14 @@ def _prefill_then_decode(sata, q, k, v, n, P, chunk, dtype, heads):
     """Prefill tokens [0, n), decode the rest one step at a time; check the
     listed (b, h) heads: every prefill row, every decoded row and both states."""
     dev = lambda a: to_dev(a, dtype)
+    B, H = q.shape[:2]
+    d = q.shape[-1]
+    ops = operands(sata, dtype, B, H, n, d, v.shape[-1], P, chunk)
     y, S = sata.prefill(dev(q[:, :, :n]), dev(k[:, :, :n]), dev(v[:, :, :n]), P, chunk)
     torch.cuda.synchronize()
     for b, h in heads:
         check_prefill_head(to_host(y[b, h]), to_host(S[b, h]), q[b, h, :n], k[b, h, :n], v[b, h, :n], P,
-                           dtype, f"prefill b{b} h{h}")
+                           ops, dtype, chunk, f"prefill b{b} h{h}")
     del y
     steps = q.shape[2] - n
     ys = []
@@ -48,10 +50,8 @@ def _prefill_then_decode(sata, q, k, v, n, P, chunk, dtype, heads):
     for b, h in heads:
         yr, _, kap = oracle.taylor_attention_rows(q[b, h], k[b, h], v[b, h], P, list(range(n, n + steps)))
         got = np.stack([to_host(yy[b, h]) for yy in ys])
-        err, _ = max_row_rel_error(got, yr, kap)
-        assert err <= TOL[dtype], f"decode b{b} h{h}: {err:.3e}"
-        s_err = state_rel_error(to_host(S[b, h]), oracle.state_ref(k[b, h], v[b, h], P))
-        assert s_err <= TOL[dtype], f"decode state b{b} h{h}: {s_err:.3e}"
+        check_rows(got, yr, kap, y_tol(ops, dtype), P, f"decode b{b} h{h}")
+        check_state(to_host(S[b, h]), k[b, h], v[b, h], P, ops, n, chunk, f"decode state b{b} h{h}", steps=steps)
     return S
 
 

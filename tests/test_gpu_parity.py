@@ -1,10 +1,12 @@
 """GPU parity: every hot-path call through the C ABI against the float64 oracle.
 
-Inputs are the seeded synthetic N(0,1) tensors of sata_synth.  Floating-point
-results must match the oracle within relative error 1e-4 (float32 inputs) or
-2e-2 (bfloat16 inputs, float32 state): per query row ||y - y_ref|| / ||y_ref||
-over rows whose denominator does not cancel (kappa <= 100), and
-||S - S_ref||_F / ||S_ref||_F for the state.
+Inputs are the seeded synthetic N(0,1) tensors of sata_synth.  Per query row,
+||y - y_ref|| / ||y_ref|| must be within 2e-2 where the state contractions take
+bfloat16 operands, 1e-4 with float32 arithmetic and output, 2^-8 with float32
+arithmetic and a bfloat16 output, over rows whose denominator does not cancel
+(kappa <= 100; none may be left out at odd P).  States are compared element
+by element against the bound that the path's arithmetic allows
+(oracle.metrics.state_tol).
 """
 import sys
 
@@ -13,8 +15,9 @@ import pytest
 
 import oracle
 import sata_synth as syn
-from gpu_util import TOL, check_prefill_head, to_dev, to_host
-from oracle.metrics import max_row_rel_error, state_rel_error
+from gpu_util import (check_prefill_head, check_rows, check_state, check_state_against, operands, to_dev, to_host,
+                      y_tol)
+from oracle.metrics import max_row_rel_error
 
 pytestmark = pytest.mark.gpu
 
@@ -83,10 +86,12 @@ PREFILL_CASES = [
 def test_prefill_matches_oracle(sata, case):
     workload, B, H, n, dk, dv, P, chunk, dtype = case
     _say(f"prefill {case}")
+    ops = operands(sata, dtype, B, H, n, dk, dv, P, chunk)
     q, k, v, y, S = _run_prefill(sata, *case)
     for b in range(B):
         for h in range(H):
-            check_prefill_head(y[b, h], S[b, h], q[b, h], k[b, h], v[b, h], P, dtype, f"{case} b{b} h{h}")
+            check_prefill_head(y[b, h], S[b, h], q[b, h], k[b, h], v[b, h], P, ops, dtype, chunk,
+                               f"{case} {ops} b{b} h{h}")
 
 
 def test_prefill_empty_sequence_zeroes_state(sata):
@@ -108,13 +113,40 @@ def test_prefill_deterministic(sata):
 
 
 def test_prefill_chunk_invariance(sata):
+    """The chunk size changes only the rounding: float32 path, d = 8."""
     q, k, v = syn.make_qkv(21, 1, 1, 300, 8, 8, "f32")
     outs = [sata.prefill(*(to_dev(a, "f32") for a in (q, k, v)), 4, c) for c in (16, 32, 64, 128)]
     torch.cuda.synchronize()
     y0, S0 = to_host(outs[0][0]), to_host(outs[0][1])
+    S_abs = oracle.state_abs_ref(k[0, 0], v[0, 0], 4)
     for y, S in outs[1:]:
         assert max_row_rel_error(to_host(y)[0, 0], y0[0, 0])[0] < 1e-5
-        assert state_rel_error(to_host(S), S0) < 1e-5
+        check_state_against(to_host(S)[0, 0], S0[0, 0], S_abs, 2e-5, "chunk invariance")
+
+
+@pytest.mark.parametrize("d", [16, 32])
+def test_prefill_chunk_invariance_matrix_cores(sata, d):
+    """bf16, P = 4 on the matrix-core kernels: chunks 32, 64 and 128 (served by
+    different kernel variants) each match the oracle, and agree with each
+    other within the bfloat16-operand bounds."""
+    B, H, n, P = 1, 2, 300, 4
+    q, k, v = syn.make_qkv(28 + d, B, H, n, d, d, "bf16")
+    res = {}
+    for c in (32, 64, 128):
+        ops = operands(sata, "bf16", B, H, n, d, d, P, c)
+        assert ops == "bf16", f"chunk {c} is expected on the matrix cores"
+        y, S = sata.prefill(*(to_dev(a, "bf16") for a in (q, k, v)), P, c)
+        torch.cuda.synchronize()
+        res[c] = (to_host(y), to_host(S))
+        for h in range(H):
+            check_prefill_head(res[c][0][0, h], res[c][1][0, h], q[0, h], k[0, h], v[0, h], P, ops, "bf16", c,
+                               f"d{d} chunk {c} h{h}")
+    for h in range(H):
+        S_abs = oracle.state_abs_ref(k[0, h], v[0, h], P)
+        for c in (32, 128):
+            assert max_row_rel_error(res[c][0][0, h], res[64][0][0, h])[0] < 2 * y_tol("bf16", "bf16")
+            check_state_against(res[c][1][0, h], res[64][1][0, h], S_abs, 2 * oracle.state_tol("bf16", n, c, P),
+                                f"d{d} chunk {c} vs 64 h{h}")
 
 
 def test_prefill_rejects_bad_chunk(sata):
@@ -137,6 +169,7 @@ def test_decode_continues_prefill(sata, B, H, n1, n2, d, P, dtype):
         _, S = sata.prefill(dev(q[:, :, :n1]), dev(k[:, :, :n1]), dev(v[:, :, :n1]), P, 32)
     else:
         S = torch.zeros(B, H, D, d + 1, device="cuda")
+    ops = operands(sata, dtype, B, H, max(n1, 1), d, d, P, 32) if n1 > 0 else "f32"
     ys = []
     for t in range(n1, n1 + n2):
         ys.append(to_host(sata.decode_step(S, dev(q[:, :, t].copy()), dev(k[:, :, t].copy()),
@@ -147,10 +180,8 @@ def test_decode_continues_prefill(sata, B, H, n1, n2, d, P, dtype):
         for h in range(H):
             yr, _, kap = oracle.taylor_attention_rows(q[b, h], k[b, h], v[b, h], P, list(range(n1, n1 + n2)))
             got = np.stack([yy[b, h] for yy in ys])
-            err, _ = max_row_rel_error(got, yr, kap)
-            assert err <= TOL[dtype], f"b{b} h{h}: {err:.3e}"
-            s_err = state_rel_error(S_host[b, h], oracle.state_ref(k[b, h], v[b, h], P))
-            assert s_err <= TOL[dtype], f"state b{b} h{h}: {s_err:.3e}"
+            check_rows(got, yr, kap, y_tol(ops, dtype), P, f"b{b} h{h}")
+            check_state(S_host[b, h], k[b, h], v[b, h], P, ops, n1, 32, f"state b{b} h{h}", steps=n2)
 
 
 def test_decode_large_state_slices(sata):
@@ -168,7 +199,15 @@ def test_decode_large_state_slices(sata):
     for h in range(H):
         yr, Sr = oracle.decode_ref(S0[0, h], q[0, h, :1], k[0, h, :1], v[0, h, :1], P)
         assert max_row_rel_error(y[0, h][None], yr)[0] < 1e-4
-        assert state_rel_error(to_host(S)[0, h], Sr) < 1e-6
+        _check_decoded_state(to_host(S)[0, h], S0[0, h], Sr, k[0, h, :1], v[0, h, :1], P, f"h{h}")
+
+
+def _check_decoded_state(S_gpu, S0, Sr, k, v, P, label):
+    """A state that started from S0 (not a sum of tokens) and took len(k)
+    decode steps: each entry is off by at most a few float32 roundings of
+    |S0| plus the magnitudes of the added terms."""
+    S_abs = np.abs(np.asarray(S0, np.float64)) + oracle.state_abs_ref(k, v, P)
+    check_state_against(S_gpu, Sr, S_abs, oracle.state_tol("f32", 0, 1, P, steps=len(k)), label)
 
 
 def _random_state(rng, B, H, D, dv):
@@ -196,8 +235,9 @@ def test_decode_shapes_interleaved_on_one_stream(sata):
         for b in range(B):
             for h in range(H):
                 yr, Sr = oracle.decode_ref(S0[b, h], q[b, h, :1], k[b, h, :1], v[b, h, :1], P)
-                assert max_row_rel_error(y[b, h][None], yr)[0] < TOL[dtype], f"case {i} b{b} h{h}"
-                assert state_rel_error(S_host[b, h], Sr) < 1e-6, f"case {i} state b{b} h{h}"
+                assert max_row_rel_error(y[b, h][None], yr)[0] < y_tol("f32", dtype), f"case {i} b{b} h{h}"
+                _check_decoded_state(S_host[b, h], S0[b, h], Sr, k[b, h, :1], v[b, h, :1], P,
+                                     f"case {i} state b{b} h{h}")
 
 
 def test_decode_unaligned_state(sata):
@@ -217,7 +257,7 @@ def test_decode_unaligned_state(sata):
     for h in range(H):
         yr, Sr = oracle.decode_ref(S0[0, h], q[0, h, :1], k[0, h, :1], v[0, h, :1], P)
         assert max_row_rel_error(y[0, h][None], yr)[0] < 1e-4
-        assert state_rel_error(to_host(S)[0, h], Sr) < 1e-6
+        _check_decoded_state(to_host(S)[0, h], S0[0, h], Sr, k[0, h, :1], v[0, h, :1], P, f"h{h}")
 
 
 def test_decode_unaligned_large_state(sata):
@@ -240,7 +280,7 @@ def test_decode_unaligned_large_state(sata):
     for h in range(H):
         yr, Sr = oracle.decode_ref(S0[0, h], q[0, h, :1], k[0, h, :1], v[0, h, :1], P)
         assert max_row_rel_error(y[0, h][None], yr)[0] < 1e-4
-        assert state_rel_error(Sh[0, h], Sr) < 1e-6
+        _check_decoded_state(Sh[0, h], S0[0, h], Sr, k[0, h, :1], v[0, h, :1], P, f"h{h}")
 
 
 def test_decode_many_pieces_per_head(sata):
@@ -261,5 +301,26 @@ def test_decode_many_pieces_per_head(sata):
     for h in range(H):
         yr, Sr = oracle.decode_ref(S0[0, h], q[0, h, :2], k[0, h, :2], v[0, h, :2], P)
         got = np.stack([yy[0, h] for yy in ys])
-        assert max_row_rel_error(got, yr)[0] < TOL["bf16"]
-        assert state_rel_error(Sh[0, h], Sr) < 1e-6
+        assert max_row_rel_error(got, yr)[0] < y_tol("f32", "bf16")
+        _check_decoded_state(Sh[0, h], S0[0, h], Sr, k[0, h, :2], v[0, h, :2], P, f"h{h}")
+
+
+def test_state_host_round_trip_resumes_bit_identically(sata, tmp_path):
+    """Checkpoint and resume: a prefill's state copied to host memory, written
+    to a file, read back and copied to a new device tensor continues the
+    decode with bitwise the same outputs and states as the original."""
+    B, H, n, steps, d, P = 1, 3, 130, 3, 32, 4
+    q, k, v = syn.make_qkv(70, B, H, n + steps, d, d, "bf16")
+    dev = lambda a: to_dev(np.ascontiguousarray(a), "bf16")
+    _, S = sata.prefill(dev(q[:, :, :n]), dev(k[:, :, :n]), dev(v[:, :, :n]), P, 64)
+    torch.cuda.synchronize()
+    path = tmp_path / "state.npy"
+    np.save(path, S.cpu().numpy())
+    S2 = torch.from_numpy(np.load(path)).cuda()
+    assert torch.equal(S, S2)
+    for t in range(n, n + steps):
+        args = [dev(a[:, :, t]) for a in (q, k, v)]
+        y1 = sata.decode_step(S, *args, P)
+        y2 = sata.decode_step(S2, *args, P)
+        torch.cuda.synchronize()
+        assert torch.equal(y1, y2) and torch.equal(S, S2), f"step {t}"
