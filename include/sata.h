@@ -125,6 +125,33 @@ sata_status sata_decode_step(float* S, const void* q, const void* k, const void*
                              sata_dtype dt, int B, int H, int d_k, int d_v, int P,
                              void* y, void* stream);
 
+/* Elements of one head's residual array for sata_decode_step_compensated:
+ * D + (d_k+1)*d_v with D = C(d_k+P-1, P-1).  Host only.  -1 on invalid
+ * arguments or overflow. */
+int64_t sata_residual_elems(int d_k, int d_v, int P);
+
+/* sata_decode_step with compensated summation of the state entries that stop
+ * registering their per-token increments first as the context grows.  The
+ * paper's decode costs the same for every token however long the context
+ * (Sec. 1, Sec. 3.2); a float32 entry that grows with every token, such as
+ * the degree-0 normaliser (the token count), absorbs increments below half
+ * its ulp once about 2^24 tokens have been summed, so the outputs drift from
+ * the method's.  This call keeps those entries as unevaluated float pairs:
+ *   R : [B][H][D + (d_k+1)*d_v] float32 (device, read and written in place),
+ *       per head R[f] for the normaliser column of row f (all D rows), then
+ *       R[D + f*d_v + j] for value column j of rows f <= d_k (degrees 0 and 1).
+ *       Zero it when the state is created (sata_prefill's state needs no
+ *       residual: it adds whole chunks at a time).
+ * After each call S holds the rounded pair sums, so S alone is the state to
+ * float32 accuracy and may also be passed to sata_decode_step; the other
+ * entries are updated as there.  The extra traffic is 8 bytes per residual
+ * per step (3.5% of the state traffic at d_k = d_v = 32, P = 4).
+ * SATA_ERR_UNSUPPORTED unless S is 16-byte aligned and d_v <= 127;
+ * SATA_ERR_INVALID_ARG for a NULL R; otherwise as sata_decode_step. */
+sata_status sata_decode_step_compensated(float* S, float* R, const void* q, const void* k, const void* v,
+                                         sata_dtype dt, int B, int H, int d_k, int d_v, int P,
+                                         void* y, void* stream);
+
 /* One decode step with grouped query heads: each of the B*H_kv key/value
  * heads keeps one state and serves G consecutive query heads (query head
  * g + G*h reads key/value head h).  Sharing one key/value head among several

@@ -52,6 +52,10 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.sata_prefill_operands.restype = i32
     lib.sata_decode_step.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp]
     lib.sata_decode_step.restype = i32
+    lib.sata_residual_elems.argtypes = [i32, i32, i32]
+    lib.sata_residual_elems.restype = i64
+    lib.sata_decode_step_compensated.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp]
+    lib.sata_decode_step_compensated.restype = i32
     lib.sata_decode_step_grouped.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp, vp]
     lib.sata_decode_step_grouped.restype = i32
     lib.sata_status_string.argtypes = [i32]
@@ -244,6 +248,42 @@ def decode_step(S, q, k, v, P: int, y=None):
     with torch.cuda.device(q.device):
         _check(load_library().sata_decode_step(_ptr(S), _ptr(q), _ptr(k), _ptr(v), code, B, H, dk, dv, P,
                                                _ptr(y), _stream_ptr()), "sata_decode_step")
+    return y
+
+
+def residual_elems(d_k: int, d_v: int, P: int) -> int:
+    return int(load_library().sata_residual_elems(d_k, d_v, P))
+
+
+def decode_step_compensated(S, R, q, k, v, P: int, y=None):
+    """decode_step with compensated summation of the normaliser column and the
+    degree-0/1 rows: R [B, H, residual_elems(d_k, d_v, P)] float32, zero when
+    the state is created, updated in place with S.  Returns y [B, H, d_v]."""
+    torch = _torch()
+    code = _dtype_code(q)
+    _check_same_dtype(q, k=k, v=v)
+    if q.dim() != 3 or v.dim() != 3:
+        raise ValueError("q, k, v must be [B, H, d]")
+    B, H, dk = q.shape
+    dv = v.shape[-1]
+    _check_shape(k, "k", (B, H, dk))
+    _check_shape(v, "v", (B, H, dv))
+    _check_state(S, (B, H, _features(dk, P), dv + 1))
+    if R.dtype != torch.float32:
+        raise TypeError("R must be float32")
+    _check_shape(R, "R", (B, H, residual_elems(dk, dv, P)))
+    if y is not None:
+        _check_same_dtype(q, y=y)
+        _check_shape(y, "y", (B, H, dv))
+    for name, t in (("S", S), ("R", R), ("q", q), ("k", k), ("v", v)):
+        _check_tensor(t, name, q.device)
+    if y is None:
+        y = torch.empty(B, H, dv, dtype=q.dtype, device=q.device)
+    _check_tensor(y, "y", q.device)
+    with torch.cuda.device(q.device):
+        _check(load_library().sata_decode_step_compensated(_ptr(S), _ptr(R), _ptr(q), _ptr(k), _ptr(v), code, B, H,
+                                                           dk, dv, P, _ptr(y), _stream_ptr()),
+               "sata_decode_step_compensated")
     return y
 
 

@@ -26,10 +26,10 @@ namespace sata {
 namespace {
 
 constexpr int kGroupedUnroll = 2;
-// Share of a head's stream given to the piece on an even-numbered XCD (the
-// hardware deals workgroups to the 8 XCDs in turn; odd ones stream this
-// pattern about a quarter more slowly).
-constexpr double kGroupedEvenShare = 0.557;
+// The share of a head's stream given to the piece on an even-numbered XCD
+// comes from xcd_even_share(): on MI355X the hardware deals workgroups to the
+// 8 XCDs in turn and odd ones stream this pattern about a quarter more slowly;
+// other devices split evenly.
 
 __device__ __forceinline__ void lds_wait_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
@@ -69,7 +69,7 @@ __global__ void __launch_bounds__(NTH, (G <= 2 ? 8 : 4))
 decode_grouped_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __restrict__ k,
                       const T* __restrict__ v, T* __restrict__ y, const uint64_t* __restrict__ packed,
                       const float* __restrict__ weight, int64_t D, int dk, int dv, int tu, int npieces, int steps,
-                      int max_rows, float* __restrict__ xpart, int* __restrict__ cnt) {
+                      int max_rows, float* __restrict__ xpart, int* __restrict__ cnt, float even_share) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
   const int E = dv + 1;
   const int tid = threadIdx.x;
@@ -77,7 +77,7 @@ decode_grouped_kernel(float* __restrict__ S, const T* __restrict__ q, const T* _
   const int piece = __builtin_amdgcn_readfirstlane((int)(blockIdx.x % (unsigned)npieces));
   const int64_t bh = __builtin_amdgcn_readfirstlane((int)(blockIdx.x / (unsigned)npieces));  // key/value head
   auto step_of = [&](int p) -> int64_t {
-    const float w = (float)(p >> 1) + ((p & 1) ? (float)kGroupedEvenShare : 0.0f);
+    const float w = (float)(p >> 1) + ((p & 1) ? even_share : 0.0f);
     return (int64_t)(w * 2.0f / (float)npieces * (float)steps + 0.5f);
   };
   const int64_t m_lo = (piece == 0) ? 0 : step_of(piece);
@@ -284,6 +284,7 @@ GroupedDecodePlan plan_decode_grouped(int64_t D, int dk, int dv, int BH, int G) 
   GroupedDecodePlan p;
   const int E = dv + 1;
   if (G != 2 && G != 4 && G != 8) return p;
+  p.even_share = xcd_even_share();
   const int nth = (D * E <= 65536 && 8 * E <= 256) ? 256 : 1024;
   const int unit = E / std::gcd(E, 4);
   const int tu = (nth / unit) * unit;
@@ -299,7 +300,8 @@ GroupedDecodePlan plan_decode_grouped(int64_t D, int dk, int dv, int BH, int G) 
   // while the pieces' feature values do not fit in LDS
   auto rows_for = [&](int npc) -> int64_t {
     if (npc == 1) return D;
-    const int64_t piece_steps = (int64_t)(kGroupedEvenShare * 2.0 / npc * (double)steps) + 2;
+    const double share = std::max(p.even_share, 1.0f - p.even_share);
+    const int64_t piece_steps = (int64_t)(share * 2.0 / npc * (double)steps) + 2;
     return std::min<int64_t>(D, (4 * tu * piece_steps + 3) / E + 3);
   };
   int64_t rows = rows_for(np);
@@ -333,7 +335,7 @@ hipError_t launch_decode_grouped(float* S, const void* q, const void* k, const v
     if (e != hipSuccess) return e;                                                                            \
     hipLaunchKernelGGL((decode_grouped_kernel<TT, NTH, GG>), dim3((unsigned)BH * (unsigned)plan.np), dim3(NTH), \
                        plan.lds, s, S, (const TT*)q, (const TT*)k, (const TT*)v, (TT*)y, t.packed, t.weight, t.D,   \
-                       dk, dv, plan.tu, plan.np, plan.steps, plan.rows, partial, counters);                   \
+                       dk, dv, plan.tu, plan.np, plan.steps, plan.rows, partial, counters, plan.even_share);  \
   } while (0)
 #define SATA_DECODE_GROUPED_G(TT, NTH)                  \
   do {                                                  \

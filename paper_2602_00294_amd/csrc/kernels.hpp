@@ -30,14 +30,21 @@ struct DecodePlan {
   int flat_np = 1;      // workgroups (pieces) per head
   int flat_steps = 0;   // float4 steps per thread over a whole head
   int flat_rows = 0;    // state rows a piece touches at most (its feature values in LDS)
+  float even_share = 0.5f;  // share of each (even, odd) pair of pieces streamed by the even one
 };
 DecodePlan plan_decode(int64_t D, int dk, int dv, int BH);
 // partial: BH * n * (dv + 1) floats with n = nslices when nslices > 1 and the
 // state is not 16-byte aligned, n = flat_np when flat_np > 1; counters: BH
 // ints, all zero, when flat_np > 1 (the kernel leaves them zero).
+// R (may be null): per head D + (dk + 1) * dv float32 residuals of the
+// compensated entries (normaliser column, degree-0 and degree-1 rows); only
+// the flat kernel takes them (decode_supports_residuals).
 hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, void* y, bool bf16,
                          int BH, int dk, int dv, const DevTable& t, const DecodePlan& plan,
-                         float* partial, int* counters, hipStream_t s);
+                         float* partial, int* counters, hipStream_t s, float* R = nullptr);
+bool decode_supports_residuals(const DecodePlan& plan, const float* S);
+// Share of each (even, odd) pair of decode pieces for the even one on the current device.
+float xcd_even_share();
 
 // ---- decode step, grouped query heads ------------------------------------------
 struct GroupedDecodePlan {
@@ -48,6 +55,7 @@ struct GroupedDecodePlan {
   int steps = 0;   // float4 steps per thread over a whole head
   int rows = 0;    // state rows a piece touches at most
   int G = 0;       // query heads per key/value head (2, 4 or 8)
+  float even_share = 0.5f;  // share of each (even, odd) pair of pieces streamed by the even one
 };
 GroupedDecodePlan plan_decode_grouped(int64_t D, int dk, int dv, int BH, int G);
 // BH key/value heads; S 16-byte aligned; partial: BH * np * G * (dv + 1)

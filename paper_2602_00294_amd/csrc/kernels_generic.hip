@@ -14,7 +14,9 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
+#include <cstring>
 #include <numeric>
 
 #include "device_common.hpp"
@@ -150,28 +152,61 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(
 //
 // With npieces > 1 (an even number), each head is streamed by that many
 // workgroups (blockIdx = npieces head + piece), piece p taking a thread's
-// steps [m(p), m(p+1)).  The hardware deals workgroups to the 8 XCDs in turn,
-// so even pieces run on even-numbered XCDs and odd pieces on odd ones, which
-// stream this pattern about a quarter more slowly: of each (even, odd) pair
-// the even piece takes the share kFlatEvenShare of the steps.  Each piece
+// steps [m(p), m(p+1)).  On MI355X the hardware deals workgroups to the 8 XCDs
+// in turn, so even pieces run on even-numbered XCDs and odd pieces on odd
+// ones, which stream this pattern about a quarter more slowly: of each (even,
+// odd) pair the even piece takes the share `even_share` of the steps (0.557
+// there; 0.5 on any other device, where that dispatch pattern is not
+// assumed).  Any share gives the same result; it only balances time.  Each piece
 // needs the features of its own rows only, kept in LDS from its first row on.
 // Each piece stores its E column sums at xpart[npieces head + piece] with
 // device-coherent stores and bumps cnt[head]; the last to arrive adds them in
 // piece order (so the result does not depend on the order of arrival), writes
 // y and sets the counter back to 0.  No device-scope fence is used: one would
 // write back the XCD's whole L2, full of freshly written state.
+//
+// Compensated variant (COMP): R holds, per head, the float32 rounding
+// residuals of the entries whose per-token increments are the first to fall
+// below half an ulp of a long sum (the normaliser column of every row, and
+// the value columns of the degree-0 and degree-1 rows; see comp_index).
+// Those entries are updated as an unevaluated float pair (S, R) by exact
+// two-sums, and S is renormalised to the rounded pair sum, so S alone keeps
+// float32 accuracy however many tokens have been added.  Their residuals are
+// loaded with the state, kFlatUnroll steps ahead.
 constexpr int kFlatUnroll = 2;
-// Share of a head's stream given to the piece on an even-numbered XCD: their
-// measured streaming times for this pattern are 47 and 59 us per head.
-constexpr double kFlatEvenShare = 0.557;
+// Share of a head's stream given to the piece on an even-numbered XCD of
+// MI355X: their measured streaming times for this pattern are 47 and 59 us
+// per head.
+constexpr float kMi355EvenShare = 0.557f;
 
-template <typename T, int NTH>
-__global__ void __launch_bounds__(NTH, 8)
+// Residual slot of state entry (row f, column j) of a head, or -1 when the
+// entry is not compensated: the normaliser column j = dv of every row at
+// [f], the value columns of rows f <= dk (degrees 0 and 1) at [D + f dv + j].
+// (Rows and slots fit in 32 bits: D <= 2^26 and dk, dv <= 255.)
+__device__ __forceinline__ int comp_index(int f, int j, int D, int dk, int dv) {
+  return (j == dv) ? f : ((f <= dk) ? D + f * dv + j : -1);
+}
+
+// (s, r) += a for an unevaluated pair s + r: two exact two-sums (Knuth), the
+// second folding the residual back so that s is the pair's rounded value.
+__device__ __forceinline__ void comp_add(float& s, float& r, float a) {
+  const float t = s + a;
+  const float tp = t - s;
+  const float e = (s - (t - tp)) + (a - tp);  // s + a = t + e exactly
+  const float r1 = r + e;
+  const float u = t + r1;
+  const float up = u - t;
+  r = (t - (u - up)) + (r1 - up);  // t + r1 = u + r exactly
+  s = u;
+}
+
+template <typename T, int NTH, bool COMP>
+__global__ void __launch_bounds__(NTH, COMP ? 4 : 8)
 decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __restrict__ k,
                    const T* __restrict__ v, T* __restrict__ y, const uint64_t* __restrict__ packed,
                    const float* __restrict__ weight, int64_t D, int dk, int dv, int tu, int P, int closed,
                    float xscale, int npieces, int steps, int max_rows, float* __restrict__ xpart,
-                   int* __restrict__ cnt) {
+                   int* __restrict__ cnt, float* __restrict__ R, float even_share) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
   const int E = dv + 1;
   const int tid = threadIdx.x;
@@ -180,13 +215,14 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
   const int64_t bh = (int64_t)(blockIdx.x / (unsigned)npieces);
   // the piece's steps: the first piece starts at 0 and the last runs to the end
   auto step_of = [&](int p) -> int64_t {
-    const float w = (float)(p >> 1) + ((p & 1) ? (float)kFlatEvenShare : 0.0f);
+    const float w = (float)(p >> 1) + ((p & 1) ? even_share : 0.0f);
     return (int64_t)(w * 2.0f / (float)npieces * (float)steps + 0.5f);
   };
   const int64_t m_lo = (piece == 0) ? 0 : step_of(piece);
   const int64_t m_hi = (piece == npieces - 1) ? ((int64_t)1 << 40) : step_of(piece + 1);
   const int64_t N = D * E;
   float* const Sh = S + bh * N;
+  float* const Rh = COMP ? R + bh * (D + (int64_t)(dk + 1) * dv) : nullptr;
   float2* const fkq = (float2*)lds;        // [max_rows] {phi_k, phi_q} of rows row_lo..
   float* const xq = (float*)(fkq + max_rows);  // [dk]
   float* const xk = xq + dk;               // [dk]
@@ -314,33 +350,67 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
     const int64_t f = le / E;
     const int j = (int)(le - f * E);
     const float2 fw = fkq[f - row_lo];
-    lx += fw.x * ve[j];
+    const int ri = COMP ? comp_index((int)f, j, (int)D, dk, dv) : -1;
+    if (COMP && ri >= 0) {
+      float r = Rh[ri];
+      comp_add(lx, r, __fmul_rn(fw.x, ve[j]));
+      Rh[ri] = r;
+    } else {
+      lx += fw.x * ve[j];
+    }
     Sh[le] = lx;
     lo_val[lt] = fw.y * lx;
     lo_col[lt] = j;
   }
 
-  // this thread's four lanes: rows f0[c] + rps m, columns jc[c]
+  // this thread's four lanes: rows fr[c] + rps m (f0[c] + rps m counted from
+  // the piece's first row), columns jc[c]
   const int rps = 4 * tu / E;
-  int f0[4];
+  int f0[4], jc[4], fr[4];
   float vj[4], acc[4];
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
     const int e = a0 + 4 * tid + c;
-    f0[c] = e / E;
-    vj[c] = ve[e - f0[c] * E];
+    fr[c] = e / E;
+    jc[c] = e - fr[c] * E;
+    f0[c] = fr[c] - (int)row_lo;
+    vj[c] = ve[jc[c]];
     acc[c] = 0.0f;
-    f0[c] -= (int)row_lo;  // positions in the piece's feature rows
+  }
+  // residuals of the compensated lanes of the first kFlatUnroll steps (COMP only)
+  float rc[kFlatUnroll][4];
+#pragma unroll
+  for (int u = 0; u < kFlatUnroll; ++u) {
+    const int64_t g = tid + (int64_t)tu * (m_lo + u);
+    const bool ok = active && g < nv && m_lo + u < m_hi;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      rc[u][c] = 0.0f;
+      if (COMP) {
+        const int ri = comp_index(fr[c] + rps * (int)(m_lo + u), jc[c], (int)D, dk, dv);
+        if (ok && ri >= 0) rc[u][c] = Rh[ri];
+      }
+    }
   }
   float4* const Sw = (float4*)(Sh + a0);
   if (active) {
     for (int64_t m0 = m_lo;; m0 += kFlatUnroll) {
       float4 nxt[kFlatUnroll];
+      float rn[kFlatUnroll][4];
 #pragma unroll
       for (int u = 0; u < kFlatUnroll; ++u) {
         const int64_t m = m0 + kFlatUnroll + u;
         const int64_t g = tid + (int64_t)tu * m;
-        nxt[u] = (g < nv && m < m_hi) ? Sv[g] : float4{0.0f, 0.0f, 0.0f, 0.0f};
+        const bool ok = g < nv && m < m_hi;
+        nxt[u] = ok ? Sv[g] : float4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          rn[u][c] = 0.0f;
+          if (COMP) {
+            const int ri = comp_index(fr[c] + rps * (int)m, jc[c], (int)D, dk, dv);
+            if (ok && ri >= 0) rn[u][c] = Rh[ri];
+          }
+        }
       }
       bool more = false;
 #pragma unroll
@@ -352,13 +422,22 @@ decode_flat_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __re
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
             const float2 fw = fkq[f0[c] + rps * m];
-            x[c] += fw.x * vj[c];
+            const int ri = COMP ? comp_index(fr[c] + rps * (int)m, jc[c], (int)D, dk, dv) : -1;
+            if (COMP && ri >= 0) {
+              float r = rc[u][c];
+              comp_add(x[c], r, __fmul_rn(fw.x, vj[c]));
+              Rh[ri] = r;
+            } else {
+              x[c] += fw.x * vj[c];
+            }
             acc[c] += fw.y * x[c];
           }
           Sw[g] = float4{x[0], x[1], x[2], x[3]};
           more = true;
         }
         cur[u] = nxt[u];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) rc[u][c] = rn[u][c];
       }
       if (!more) break;
     }
@@ -640,6 +719,10 @@ __global__ void fill_zero_kernel(float* p, int64_t count) {
 
 // ---------------------------------------------------------------- launchers
 
+bool decode_supports_residuals(const DecodePlan& plan, const float* S) {
+  return plan.flat_tu > 0 && ((uintptr_t)S & 15) == 0;
+}
+
 hipError_t launch_fill_zero(float* p, int64_t count, hipStream_t s) {
   if (count <= 0) return hipSuccess;
   const int64_t blocks = std::min<int64_t>((count + kThreads - 1) / kThreads, 16384);
@@ -671,9 +754,30 @@ hipError_t launch_feature_map(const void* x, bool bf16, int64_t rows, const DevT
   return hipSuccess;
 }
 
+// Share of each (even, odd) pair of decode pieces given to the even one: the
+// MI355X value where the device is one (gfx950 with 256 compute units, whose
+// workgroups go to its 8 XCDs in turn), an even split on any other device.
+// Looked up once per device.
+float xcd_even_share() {
+  static std::atomic<int> cache[64];  // 0: unknown, 1: MI355X, 2: other
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0.5f;
+  int c = cache[dev].load(std::memory_order_relaxed);
+  if (c == 0) {
+    hipDeviceProp_t prop;
+    c = 2;
+    if (hipGetDeviceProperties(&prop, dev) == hipSuccess && prop.multiProcessorCount == 256 &&
+        std::strncmp(prop.gcnArchName, "gfx950", 6) == 0)
+      c = 1;
+    cache[dev].store(c, std::memory_order_relaxed);
+  }
+  return c == 1 ? kMi355EvenShare : 0.5f;
+}
+
 DecodePlan plan_decode(int64_t D, int dk, int dv, int BH) {
   const int E = dv + 1;
   DecodePlan p;
+  p.even_share = xcd_even_share();
   // Row-wise plans, used when the state is not 16-byte aligned: a head whose
   // feature values fit in LDS is streamed by one workgroup, a larger one in
   // feature slices of about 32K state elements (128 KB of float32) with a
@@ -709,7 +813,8 @@ DecodePlan plan_decode(int64_t D, int dk, int dv, int BH) {
   // rounding) times 4 tu elements, and the rows cut at both ends
   int64_t rows = D;
   if (np > 1) {
-    const int64_t piece_steps = (int64_t)(kFlatEvenShare * 2.0 / np * (double)steps) + 2;
+    const double share = std::max(p.even_share, 1.0f - p.even_share);
+    const int64_t piece_steps = (int64_t)(share * 2.0 / np * (double)steps) + 2;
     rows = std::min<int64_t>(D, (4 * tu * piece_steps + 3) / E + 3);
   }
   const size_t lds = sizeof(float2) * (size_t)rows + sizeof(float) * (size_t)(2 * dk + E + 4 * tu + 9 * E + 16);
@@ -725,8 +830,9 @@ DecodePlan plan_decode(int64_t D, int dk, int dv, int BH) {
 
 hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, void* y, bool bf16, int BH,
                          int dk, int dv, const DevTable& t, const DecodePlan& plan, float* partial,
-                         int* counters, hipStream_t s) {
+                         int* counters, hipStream_t s, float* R) {
   const int E = dv + 1;
+  if (R != nullptr && !decode_supports_residuals(plan, S)) return hipErrorInvalidValue;
   if (plan.flat_tu > 0 && ((uintptr_t)S & 15) == 0) {
     hipError_t e;
     if (plan.flat_np > 1 && (partial == nullptr || counters == nullptr)) return hipErrorInvalidValue;
@@ -737,19 +843,22 @@ hipError_t launch_decode(float* S, const void* q, const void* k, const void* v, 
     // scales by itself.
     const int closed = (t.P == 4 && plan.flat_np <= 2) ? 1 : 0;
     const float xscale = closed ? 1.0f / std::sqrt(std::sqrt((float)dk)) : 1.0f;
-#define SATA_DECODE_FLAT(TT, NTH)                                                                         \
-  e = hipFuncSetAttribute((const void*)decode_flat_kernel<TT, NTH>,                                       \
+#define SATA_DECODE_FLAT(TT, NTH, COMP)                                                                   \
+  e = hipFuncSetAttribute((const void*)decode_flat_kernel<TT, NTH, COMP>,                                 \
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)plan.flat_lds);                \
   if (e != hipSuccess) return e;                                                                          \
-  hipLaunchKernelGGL((decode_flat_kernel<TT, NTH>), dim3((unsigned)BH * (unsigned)plan.flat_np), dim3(NTH),       \
-                     plan.flat_lds, s, S, (const TT*)q, (const TT*)k, (const TT*)v, (TT*)y, t.packed, t.weight,   \
-                     t.D, dk, dv, plan.flat_tu, t.P, closed, xscale, plan.flat_np, plan.flat_steps, plan.flat_rows, \
-                     partial, counters)
+  hipLaunchKernelGGL((decode_flat_kernel<TT, NTH, COMP>), dim3((unsigned)BH * (unsigned)plan.flat_np),         \
+                     dim3(NTH), plan.flat_lds, s, S, (const TT*)q, (const TT*)k, (const TT*)v, (TT*)y, t.packed,  \
+                     t.weight, t.D, dk, dv, plan.flat_tu, t.P, closed, xscale, plan.flat_np, plan.flat_steps,     \
+                     plan.flat_rows, partial, counters, R, plan.even_share)
+#define SATA_DECODE_FLAT_C(TT, NTH) \
+  if (R) { SATA_DECODE_FLAT(TT, NTH, true); } else { SATA_DECODE_FLAT(TT, NTH, false); }
     if (plan.flat_nth == 256) {
-      if (bf16) { SATA_DECODE_FLAT(bf16_t, 256); } else { SATA_DECODE_FLAT(float, 256); }
+      if (bf16) { SATA_DECODE_FLAT_C(bf16_t, 256); } else { SATA_DECODE_FLAT_C(float, 256); }
     } else {
-      if (bf16) { SATA_DECODE_FLAT(bf16_t, 1024); } else { SATA_DECODE_FLAT(float, 1024); }
+      if (bf16) { SATA_DECODE_FLAT_C(bf16_t, 1024); } else { SATA_DECODE_FLAT_C(float, 1024); }
     }
+#undef SATA_DECODE_FLAT_C
 #undef SATA_DECODE_FLAT
     return hipGetLastError();
   }

@@ -66,6 +66,8 @@ constexpr int64_t kMaxFeatures = (int64_t)1 << 26;
 constexpr int kMaxHeads = 65535;
 // Upper bound on the partial-readout workspace one call may use.
 constexpr size_t kMaxWorkspace = (size_t)512 << 20;
+// The flat decode kernel (the one that takes residuals) serves d_v up to this.
+constexpr int kMaxCompensatedDv = 127;
 
 sata_status get_table(int d, int P, hipStream_t stream, sata::DevTable* out) {
   int dev = 0;
@@ -191,6 +193,40 @@ PrefillPath prefill_path(sata_dtype dt, int BH, int n, int d_k, int d_v, int P, 
   if (dt == SATA_BF16 && sata::plan_prefill_mfma(BH, n, d_k, d_v, P, chunk, &mp)) return PrefillPath::kMfma32;
   if (dt == SATA_BF16 && sata::plan_prefill_blocks(BH, n, d_k, d_v, P, chunk, &mp)) return PrefillPath::kBlocks;
   return PrefillPath::kFloat32;
+}
+
+sata_status decode_step(float* S, float* R, const void* q, const void* k, const void* v, sata_dtype dt, int B,
+                        int H, int d_k, int d_v, int P, void* y, void* stream) {
+  if (!valid_dtype(dt)) return fail(SATA_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
+  if (B < 1 || H < 1) return fail(SATA_ERR_INVALID_ARG, "B=%d H=%d must be >= 1", B, H);
+  int64_t D = 0;
+  sata_status st = check_dims(d_k, d_v, P, &D);
+  if (st != SATA_OK) return st;
+  if ((int64_t)B * H > kMaxHeads) return fail(SATA_ERR_TOO_LARGE, "B*H=%lld exceeds %d", (long long)B * H, kMaxHeads);
+  if (!S || !q || !k || !v || !y) return fail(SATA_ERR_INVALID_ARG, "null tensor pointer");
+  const int BH = B * H;
+  hipStream_t s = (hipStream_t)stream;
+  sata::DecodePlan plan = sata::plan_decode(D, d_k, d_v, BH);
+  if (R && !sata::decode_supports_residuals(plan, S))
+    return fail(SATA_ERR_UNSUPPORTED, "the compensated decode needs a 16-byte aligned state and d_v <= %d",
+                kMaxCompensatedDv);
+  sata::DevTable t;
+  if ((st = get_table(d_k, P, s, &t)) != SATA_OK) return st;
+  float* partial = nullptr;
+  int* counters = nullptr;
+  // partial sums: one row per slice (row-wise path) or per piece of a head (flat path)
+  const int64_t rows = std::max<int64_t>(plan.nslices > 1 ? plan.nslices : 0, plan.flat_np > 1 ? plan.flat_np : 0);
+  if (rows > 0) {
+    void* ws = nullptr;
+    const size_t bytes = sizeof(float) * (size_t)BH * rows * (d_v + 1);
+    if ((st = get_workspace(bytes, s, &ws)) != SATA_OK) return st;
+    partial = (float*)ws;
+  }
+  if (plan.flat_np > 1 && (st = get_counters(BH, s, &counters)) != SATA_OK) return st;
+  hipError_t e =
+      sata::launch_decode(S, q, k, v, y, dt == SATA_BF16, BH, d_k, d_v, t, plan, partial, counters, s, R);
+  if (e != hipSuccess) return hip_fail(e, "decode launch");
+  return ok();
 }
 
 }  // namespace
@@ -320,33 +356,21 @@ sata_status sata_prefill(const void* q, const void* k, const void* v, sata_dtype
 
 sata_status sata_decode_step(float* S, const void* q, const void* k, const void* v, sata_dtype dt, int B,
                              int H, int d_k, int d_v, int P, void* y, void* stream) {
-  if (!valid_dtype(dt)) return fail(SATA_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
-  if (B < 1 || H < 1) return fail(SATA_ERR_INVALID_ARG, "B=%d H=%d must be >= 1", B, H);
-  int64_t D = 0;
-  sata_status st = check_dims(d_k, d_v, P, &D);
-  if (st != SATA_OK) return st;
-  if ((int64_t)B * H > kMaxHeads) return fail(SATA_ERR_TOO_LARGE, "B*H=%lld exceeds %d", (long long)B * H, kMaxHeads);
-  if (!S || !q || !k || !v || !y) return fail(SATA_ERR_INVALID_ARG, "null tensor pointer");
-  const int BH = B * H;
-  hipStream_t s = (hipStream_t)stream;
-  sata::DevTable t;
-  if ((st = get_table(d_k, P, s, &t)) != SATA_OK) return st;
-  sata::DecodePlan plan = sata::plan_decode(D, d_k, d_v, BH);
-  float* partial = nullptr;
-  int* counters = nullptr;
-  // partial sums: one row per slice (row-wise path) or per piece of a head (flat path)
-  const int64_t rows = std::max<int64_t>(plan.nslices > 1 ? plan.nslices : 0, plan.flat_np > 1 ? plan.flat_np : 0);
-  if (rows > 0) {
-    void* ws = nullptr;
-    const size_t bytes = sizeof(float) * (size_t)BH * rows * (d_v + 1);
-    if ((st = get_workspace(bytes, s, &ws)) != SATA_OK) return st;
-    partial = (float*)ws;
-  }
-  if (plan.flat_np > 1 && (st = get_counters(BH, s, &counters)) != SATA_OK) return st;
-  hipError_t e =
-      sata::launch_decode(S, q, k, v, y, dt == SATA_BF16, BH, d_k, d_v, t, plan, partial, counters, s);
-  if (e != hipSuccess) return hip_fail(e, "decode launch");
-  return ok();
+  return decode_step(S, nullptr, q, k, v, dt, B, H, d_k, d_v, P, y, stream);
+}
+
+sata_status sata_decode_step_compensated(float* S, float* R, const void* q, const void* k, const void* v,
+                                         sata_dtype dt, int B, int H, int d_k, int d_v, int P, void* y,
+                                         void* stream) {
+  if (!R) return fail(SATA_ERR_INVALID_ARG, "null residual pointer");
+  return decode_step(S, R, q, k, v, dt, B, H, d_k, d_v, P, y, stream);
+}
+
+int64_t sata_residual_elems(int d_k, int d_v, int P) {
+  if (d_k < 1 || d_v < 1 || P < 1) return -1;
+  const int64_t f = sata::feature_count(d_k, P);
+  if (f < 0) return -1;
+  return f + (int64_t)(d_k + 1) * d_v;
 }
 
 sata_status sata_decode_step_grouped(float* S, const void* q, const void* k, const void* v, sata_dtype dt, int B,
