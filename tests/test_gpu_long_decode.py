@@ -74,7 +74,7 @@ def test_compensated_decode_matches_oracle(sata, B, H, n1, n2, d, P, dtype):
             # rounding (and at most one step of the bfloat16 output rounding)
             plain = np.stack([yy[b, h] for yy in ys_plain])
             same = 1e-5 if dtype == "f32" else 2.0 ** -7
-            assert np.max(np.abs(got - plain) / np.maximum(np.abs(plain), 1e-3)) < same
+            assert np.max(oracle.row_rel_error(got, plain)) < same
             check_state(Sh[b, h], k[b, h], v[b, h], P, ops, n1, 32, f"state b{b} h{h}", steps=n2)
             # a residual is at most half an ulp of its entry (plus what it carries from the last step)
             z = Sh[b, h][:, d]
