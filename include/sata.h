@@ -125,6 +125,24 @@ sata_status sata_decode_step(float* S, const void* q, const void* k, const void*
                              sata_dtype dt, int B, int H, int d_k, int d_v, int P,
                              void* y, void* stream);
 
+/* sata_decode_step for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, kernels and results (bitwise) as
+ * sata_decode_step; it calls no hipMalloc, hipFree or allocating library
+ * routine.  The partial sums and arrival counters of the split decode live in
+ * a static 4 MB array per device, held until the process ends (the first call
+ * on a device looks up its address and clears its counters with a kernel on
+ * `stream`).  Every call on a device shares that array, so calls that overlap
+ * on one device (other streams, other threads) race; serialise them.
+ * SATA_ERR_TOO_LARGE if a call needs more than 4 MB - 256 KB of partial sums
+ * (B*H * pieces * (d_v+1) floats; 67.6 KB at B*H = 256, d_k = d_v = 32, P = 4);
+ * SATA_ERR_UNSUPPORTED if the (d_k, P) feature table does not exist on the
+ * device yet: any earlier sata_decode_step, sata_prefill or sata_feature_map
+ * call with that d_k and P creates it. */
+sata_status sata_decode_step_noalloc(float* S, const void* q, const void* k, const void* v,
+                                     sata_dtype dt, int B, int H, int d_k, int d_v, int P,
+                                     void* y, void* stream);
+
 /* Elements of one head's residual array for sata_decode_step_compensated:
  * D + (d_k+1)*d_v with D = C(d_k+P-1, P-1).  Host only.  -1 on invalid
  * arguments or overflow. */

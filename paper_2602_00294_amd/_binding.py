@@ -52,6 +52,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.sata_prefill_operands.restype = i32
     lib.sata_decode_step.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp]
     lib.sata_decode_step.restype = i32
+    lib.sata_decode_step_noalloc.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp]
+    lib.sata_decode_step_noalloc.restype = i32
     lib.sata_residual_elems.argtypes = [i32, i32, i32]
     lib.sata_residual_elems.restype = i64
     lib.sata_decode_step_compensated.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp]

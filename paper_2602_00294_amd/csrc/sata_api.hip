@@ -69,6 +69,23 @@ constexpr size_t kMaxWorkspace = (size_t)512 << 20;
 // The flat decode kernel (the one that takes residuals) serves d_v up to this.
 constexpr int kMaxCompensatedDv = 127;
 
+// Scratch of sata_decode_step_noalloc: one array per device for the life of
+// the process.  The first kScratchCounterBytes hold the per-head arrival
+// counters of the split decode (zeroed once per device by a fill kernel; the
+// kernels set each counter back to zero), the rest the pieces' partial sums.
+// In host code `scratch` names a host-side stand-in: only the address that
+// hipGetSymbolAddress returns for the current device may reach a kernel.
+constexpr size_t kScratchBytes = (size_t)4 << 20;
+constexpr size_t kScratchCounterBytes = sizeof(int) * 65536;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+struct ScratchSlot {
+  bool ready = false;
+  unsigned char* ptr = nullptr;  // the device address of `scratch` on that device
+};
+constexpr int kMaxDevices = 64;
+ScratchSlot g_scratch[kMaxDevices];  // guarded by g_mu
+
 sata_status get_table(int d, int P, hipStream_t stream, sata::DevTable* out) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -103,6 +120,53 @@ sata_status get_table(int d, int P, hipStream_t stream, sata::DevTable* out) {
   out->D = it->second.host.D;
   out->d = d;
   out->P = P;
+  return SATA_OK;
+}
+
+// The cached table of (d, P) on the current device, without creating one.
+sata_status find_table(int d, int P, sata::DevTable* out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lock(g_mu);
+  auto dc = g_devices.find(dev);
+  if (dc != g_devices.end()) {
+    auto it = dc->second.tables.find(std::make_pair(d, P));
+    if (it != dc->second.tables.end()) {
+      out->packed = it->second.packed;
+      out->weight = it->second.weight;
+      out->D = it->second.host.D;
+      out->d = d;
+      out->P = P;
+      return SATA_OK;
+    }
+  }
+  return fail(SATA_ERR_UNSUPPORTED,
+              "no feature table for d_k=%d P=%d on device %d yet: make one sata_decode_step, sata_prefill or "
+              "sata_feature_map call with these sizes first",
+              d, P, dev);
+}
+
+// The device address of `scratch` on the current device; on the first call
+// on a device it is looked up and the counter region cleared on `stream`.
+sata_status get_scratch(hipStream_t stream, unsigned char** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(SATA_ERR_UNSUPPORTED, "device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_mu);
+  ScratchSlot& slot = g_scratch[dev];
+  if (!slot.ready) {
+    void* p = nullptr;
+    if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess)
+      return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if ((e = sata::launch_fill_zero((float*)p, (int64_t)(kScratchCounterBytes / sizeof(float)), stream)) !=
+        hipSuccess)
+      return hip_fail(e, "clearing the scratch counters");
+    slot.ptr = (unsigned char*)p;
+    slot.ready = true;
+  }
+  *out = slot.ptr;
   return SATA_OK;
 }
 
@@ -357,6 +421,34 @@ sata_status sata_prefill(const void* q, const void* k, const void* v, sata_dtype
 sata_status sata_decode_step(float* S, const void* q, const void* k, const void* v, sata_dtype dt, int B,
                              int H, int d_k, int d_v, int P, void* y, void* stream) {
   return decode_step(S, nullptr, q, k, v, dt, B, H, d_k, d_v, P, y, stream);
+}
+
+sata_status sata_decode_step_noalloc(float* S, const void* q, const void* k, const void* v, sata_dtype dt, int B,
+                                    int H, int d_k, int d_v, int P, void* y, void* stream) {
+  if (!valid_dtype(dt)) return fail(SATA_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
+  if (B < 1 || H < 1) return fail(SATA_ERR_INVALID_ARG, "B=%d H=%d must be >= 1", B, H);
+  int64_t D = 0;
+  sata_status st = check_dims(d_k, d_v, P, &D);
+  if (st != SATA_OK) return st;
+  if ((int64_t)B * H > kMaxHeads) return fail(SATA_ERR_TOO_LARGE, "B*H=%lld exceeds %d", (long long)B * H, kMaxHeads);
+  if (!S || !q || !k || !v || !y) return fail(SATA_ERR_INVALID_ARG, "null tensor pointer");
+  const int BH = B * H;
+  sata::DecodePlan plan = sata::plan_decode(D, d_k, d_v, BH);
+  const int64_t rows = std::max<int64_t>(plan.nslices > 1 ? plan.nslices : 0, plan.flat_np > 1 ? plan.flat_np : 0);
+  const size_t partial_bytes = sizeof(float) * (size_t)BH * (size_t)rows * (size_t)(d_v + 1);
+  if (partial_bytes > kScratchBytes - kScratchCounterBytes)
+    return fail(SATA_ERR_TOO_LARGE, "partial sums of %zu bytes exceed the %zu-byte scratch", partial_bytes,
+                kScratchBytes - kScratchCounterBytes);
+  sata::DevTable t;
+  if ((st = find_table(d_k, P, &t)) != SATA_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  unsigned char* base = nullptr;
+  if ((st = get_scratch(s, &base)) != SATA_OK) return st;
+  float* partial = rows > 0 ? (float*)(base + kScratchCounterBytes) : nullptr;
+  int* counters = plan.flat_np > 1 ? (int*)base : nullptr;
+  hipError_t e = sata::launch_decode(S, q, k, v, y, dt == SATA_BF16, BH, d_k, d_v, t, plan, partial, counters, s);
+  if (e != hipSuccess) return hip_fail(e, "decode launch");
+  return ok();
 }
 
 sata_status sata_decode_step_compensated(float* S, float* R, const void* q, const void* k, const void* v,
