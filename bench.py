@@ -23,6 +23,9 @@ its own line in the same form:
               decode steps (the decode figure is the one that counts);
   large_d64   B=2, H=8, d_k=d_v=64, P=4 (D=47905), bf16: 4096-token prefill,
               then 1024 decode steps;
+  decode_hbm  B=16, H=32, d_k=d_v=32, P=4, bf16: a 256-token prefill, then 1024
+              decode steps over 442 MB of state, beyond the 256 MB Infinity
+              Cache (the headline's 221 MB fits in it);
   sweep_d16   B=1, H=64, d_k=d_v=16, float32, n=65536: prefill for each P in
               2..6 (the CPU leg also reports the error against softmax);
   error_study one head of 100,000 tokens, float32, for each d_k = d_v in
@@ -119,7 +122,7 @@ def parse():
     ap.add_argument("--cpu-sample-heads", type=int, default=48)
     ap.add_argument("--cpu-sample-decode-rows", type=int, default=128)
     ap.add_argument("--workload", default="headline", choices=["headline", "decode_d16", "large_d64", "sweep_d16",
-                                                                  "error_study", "context_sweep",
+                                                                  "decode_hbm", "error_study", "context_sweep",
                                                                   "decode_grouped"])
     ap.add_argument("--seq-len", type=int, default=0,
                     help="error_study only: tokens per sequence (default 100000)")
@@ -152,10 +155,22 @@ def make_inputs(dec_steps):
     return pre, dec
 
 
+def blas_threads():
+    """Threads of the BLAS library numpy uses (the oracle's matrix products)."""
+    try:
+        import threadpoolctl
+        info = [i for i in threadpoolctl.threadpool_info() if i.get("user_api") == "blas"]
+        return {i.get("internal_api", "blas"): i.get("num_threads") for i in info} or None
+    except Exception:
+        return None
+
+
 def cpu_baseline(n_heads, dec_rows, y_gpu=None):
     """Times the float64 oracle on a bounded sample of the same workload, and
     checks the GPU prefill output y_gpu ([B, H, n, d_v] on the host) against it
-    on a few rows of the first and last head."""
+    on a few rows of the first and last head; on those rows it also measures the
+    GPU output against exact float64 softmax attention, the paper's measure of
+    the approximation (log10 of the elementwise absolute difference)."""
     import numpy as np
 
     import oracle
@@ -179,15 +194,22 @@ def cpu_baseline(n_heads, dec_rows, y_gpu=None):
     pre_tok_s = (len(heads) * N) / t_pre / H
     dec_tok_s = (len(heads) * dec_rows) / t_dec / H
     parity = {}
+    soft = None
     if y_gpu is not None:
+        lds = []
+        rows = sorted({0, 63, 64, 4095, N - 1} | set(range(N - 512, N, 16)))
         for (b, h) in ((0, 0), (B - 1, H - 1)):
             q, k, v = syn.make_head(WORKLOAD_ID, b, h, N, DK, DV, "bf16")
-            rows = [0, 63, 64, 4095, N - 1]
             yr, _, kap = oracle.taylor_attention_rows(q, k, v, P, rows)
             err, _ = oracle.max_row_rel_error(y_gpu[b, h, rows], yr, kap)
             parity[f"b{b}h{h}"] = err
+            lds.append(oracle.log10_abs_diff(y_gpu[b, h, rows], oracle.softmax_attention_rows(q, k, v, rows)))
+        a = np.concatenate([x.ravel() for x in lds])
+        soft = {"P": P, "measure": "log10 |y_gpu - y_softmax| elementwise (float64 exact softmax)",
+                "rows": f"{len(rows)} rows ({rows[0]}..{rows[-1]}) of heads (0,0) and ({B - 1},{H - 1})",
+                "median": float(np.median(a)), "p99": float(np.percentile(a, 99)), "max": float(a.max())}
     return {
-        "value": None, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+        "value": None, "unit": "tokens/s", "cores": threads, "blas_threads": blas_threads(), "kind": "oracle",
         "prefill_tokens_per_s": pre_tok_s, "decode_tokens_per_s": dec_tok_s,
         "sample": (f"{len(heads)} of {B * H} heads: full {N}-token causal prefill by the direct "
                    f"float64 definition, plus {dec_rows} decode rows at positions {N}..{N + dec_rows - 1}; "
@@ -195,6 +217,7 @@ def cpu_baseline(n_heads, dec_rows, y_gpu=None):
                    f"position {N} stand in for all {B}x{H} decode rows"),
         "seconds": t_pre + t_dec,
         "parity_max_row_rel_err": parity,
+        "error_vs_softmax": soft,
     }
 
 
@@ -203,6 +226,9 @@ WORKLOADS = {
     "decode_d16": (2, 64, 32, 2048, 16, [4], "bf16", 4096),
     "large_d64": (4, 2, 8, 4096, 64, [4], "bf16", 1024),
     "sweep_d16": (5, 1, 64, 65536, 16, [2, 3, 4, 5, 6], "f32", 0),
+    # the headline head shape with twice the heads: 442 MB of state, more than
+    # the 256 MB Infinity Cache, so every decode step streams it from HBM
+    "decode_hbm": (6, 16, 32, 256, 32, [4], "bf16", 1024),
 }
 
 
@@ -300,7 +326,7 @@ def cpu_baseline_workload(wid, Bw, Hw, n, d, Ps, dt, y_gpu, pre, sata, torch):
     threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
     heads = [(0, 0), (Bw - 1, Hw - 1)]
     rows = sorted({0, 63, 64, n // 2, n - 1} | set(range(n - 96, n, 8)))
-    out = {"value": None, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+    out = {"value": None, "unit": "tokens/s", "cores": threads, "blas_threads": blas_threads(), "kind": "oracle",
            "sample": f"rows {rows[0]}..{rows[-1]} ({len(rows)} rows) of heads {heads}, direct float64 definition"}
     t = 0.0
     per_P = {}
@@ -724,6 +750,7 @@ def main():
         cb = cpu_baseline(args.cpu_sample_heads, args.cpu_sample_decode_rows, y.float().cpu().numpy())
         whole = tokens / (B * N / cb["prefill_tokens_per_s"] + B * args.decode_steps / cb["decode_tokens_per_s"])
         cb["value"] = whole
+        line["error_vs_softmax"] = cb.pop("error_vs_softmax")
         line["cpu_baseline"] = cb
     print(json.dumps(line), flush=True)
 
