@@ -105,6 +105,23 @@ sata_status sata_prefill(const void* q, const void* k, const void* v, sata_dtype
                          int B, int H, int n, int d_k, int d_v, int P, int chunk,
                          void* y, float* S_out, void* stream);
 
+/* Causal prefill with grouped query heads: each of the B*H_kv key/value heads
+ * serves G consecutive query heads (query head g + G*h reads key/value head h),
+ * the sharing of one key/value head by several query heads that a footnote of
+ * Sec. 3.3 says carries over to this formulation.  Each query head's output is
+ * sata_prefill's for its own queries and the shared keys and values:
+ *   q    : [B][H_kv*G][n][d_k], k : [B][H_kv][n][d_k], v : [B][H_kv][n][d_v]
+ *   y    : [B][H_kv*G][n][d_v], dtype dt (device, written)
+ *   S_out: [B][H_kv][D][d_v+1] float32 or NULL: each key/value head's state,
+ *          ready for sata_decode_step_grouped.
+ * G = 1 is sata_prefill.  Each member of a group runs the prefill kernels of
+ * sata_prefill with the shared keys and values, so the state contraction is
+ * repeated G times (the readouts differ per member).  B*H_kv*G <= 65535;
+ * other rules as sata_prefill. */
+sata_status sata_prefill_grouped(const void* q, const void* k, const void* v, sata_dtype dt,
+                                 int B, int H_kv, int G, int n, int d_k, int d_v, int P, int chunk,
+                                 void* y, float* S_out, void* stream);
+
 /* Precision of the operands of the state contractions that sata_prefill uses
  * for these arguments (host only, no GPU use; same validation as sata_prefill):
  * *operands = SATA_BF16 when they run on the matrix cores with bfloat16

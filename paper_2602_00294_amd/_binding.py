@@ -48,6 +48,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.sata_feature_map.restype = i32
     lib.sata_prefill.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp]
     lib.sata_prefill.restype = i32
+    lib.sata_prefill_grouped.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp]
+    lib.sata_prefill_grouped.restype = i32
     lib.sata_prefill_operands.argtypes = [i32, i32, i32, i32, i32, i32, i32, i32, ctypes.POINTER(i32)]
     lib.sata_prefill_operands.restype = i32
     lib.sata_decode_step.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp]
@@ -220,6 +222,45 @@ def prefill(q, k, v, P: int, chunk: int = 64, want_state: bool = True, y=None, S
         _check(load_library().sata_prefill(_ptr(q), _ptr(k), _ptr(v), code, B, H, n, dk, dv, P, chunk,
                                            _ptr(y), _ptr(S) if S is not None else ctypes.c_void_p(None),
                                            _stream_ptr()), "sata_prefill")
+    return y, S
+
+
+def prefill_grouped(q, k, v, P: int, chunk: int = 64, want_state: bool = True, y=None, S=None):
+    """Causal prefill with grouped query heads.  q: [B, H_q, n, d_k] with
+    H_q = G * H_kv (query head g + G*h reads key/value head h); k: [B, H_kv, n, d_k];
+    v: [B, H_kv, n, d_v].  Returns (y [B, H_q, n, d_v], S [B, H_kv, D, d_v+1] or None)."""
+    torch = _torch()
+    code = _dtype_code(q)
+    _check_same_dtype(q, k=k, v=v)
+    if q.dim() != 4 or k.dim() != 4 or v.dim() != 4:
+        raise ValueError("q [B, G*H_kv, n, d_k], k [B, H_kv, n, d_k], v [B, H_kv, n, d_v] expected")
+    B, Hq, n, dk = q.shape
+    Hkv = k.shape[1]
+    dv = v.shape[-1]
+    if Hkv < 1 or Hq % Hkv:
+        raise ValueError("the query head count must be a multiple of the key/value head count")
+    G = Hq // Hkv
+    _check_shape(k, "k", (B, Hkv, n, dk))
+    _check_shape(v, "v", (B, Hkv, n, dv))
+    D = _features(dk, P)
+    if y is not None:
+        _check_same_dtype(q, y=y)
+        _check_shape(y, "y", (B, Hq, n, dv))
+    if S is not None:
+        _check_state(S, (B, Hkv, D, dv + 1))
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check_tensor(t, name, q.device)
+    if y is None:
+        y = torch.empty(B, Hq, n, dv, dtype=q.dtype, device=q.device)
+    if want_state and S is None:
+        S = torch.empty(B, Hkv, D, dv + 1, dtype=torch.float32, device=q.device)
+    _check_tensor(y, "y", q.device)
+    if S is not None:
+        _check_tensor(S, "S", q.device)
+    with torch.cuda.device(q.device):
+        _check(load_library().sata_prefill_grouped(_ptr(q), _ptr(k), _ptr(v), code, B, Hkv, G, n, dk, dv, P, chunk,
+                                                   _ptr(y), _ptr(S) if S is not None else ctypes.c_void_p(None),
+                                                   _stream_ptr()), "sata_prefill_grouped")
     return y, S
 
 

@@ -79,7 +79,7 @@ bool plan_prefill_generic(int64_t D, int BH, int n, int dk, int dv, int chunk, s
 hipError_t launch_prefill_generic(const void* q, const void* k, const void* v, void* y, bool bf16,
                                   int BH, int n, int dk, int dv, int chunk, const DevTable& t,
                                   const PrefillGenericPlan& plan, float* S_state, float* partial,
-                                  hipStream_t s);
+                                  hipStream_t s, int qg = 1);
 
 // ---- helpers -----------------------------------------------------------------
 hipError_t launch_fill_zero(float* p, int64_t count, hipStream_t s);

@@ -532,16 +532,18 @@ __global__ void decode_finalize_kernel(const float* __restrict__ partial, T* __r
 
 // ---------------------------------------------------------------- generic prefill
 
+// q holds qg query heads per key/value head (head bh's queries at head bh * qg).
 template <typename T>
 __device__ void load_chunk(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
                            int64_t bh, int n, int t0, int cn, int C, int dk, int dv, float* xq, float* xk,
-                           float* ve) {
+                           float* ve, int qg) {
   const int E = dv + 1;
-  const int64_t qoff = (bh * n + t0) * (int64_t)dk;
+  const int64_t qoff = (bh * qg * n + t0) * (int64_t)dk;
+  const int64_t koff = (bh * n + t0) * (int64_t)dk;
   for (int i = threadIdx.x; i < C * dk; i += kThreads) {
     const int t = i / dk;
     xq[i] = t < cn ? to_f32(q[qoff + i]) : 0.0f;
-    xk[i] = t < cn ? to_f32(k[qoff + i]) : 0.0f;
+    xk[i] = t < cn ? to_f32(k[koff + i]) : 0.0f;
   }
   const int64_t voff = (bh * n + t0) * (int64_t)dv;
   for (int i = threadIdx.x; i < C * E; i += kThreads) {
@@ -558,7 +560,7 @@ __global__ void __launch_bounds__(kThreads)
 prefill_generic_main(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
                      const uint64_t* __restrict__ packed, const float* __restrict__ weight, int64_t D,
                      float* __restrict__ S_state, float* __restrict__ part, int BH, int n, int dk, int dv,
-                     int C, int FS, int seg0, int seg_len, int first_seg) {
+                     int C, int FS, int seg0, int seg_len, int first_seg, int qg) {
   // FS: features per slice, a multiple of 4 (the last slice may hold fewer, fs)
   extern __shared__ __attribute__((aligned(16))) float lds[];
   const int E = dv + 1;
@@ -587,7 +589,7 @@ prefill_generic_main(const T* __restrict__ q, const T* __restrict__ k, const T* 
   for (int t0 = seg0; t0 < seg_end; t0 += C) {
     const int cn = min(C, n - t0);
     __syncthreads();
-    load_chunk(q, k, v, bh, n, t0, cn, C, dk, dv, xq, xk, ve);
+    load_chunk(q, k, v, bh, n, t0, cn, C, dk, dv, xq, xk, ve, qg);
     __syncthreads();
     for (int i = tid; i < cn * fs; i += kThreads) {
       const int t = i / fs;
@@ -659,7 +661,7 @@ template <typename T>
 __global__ void __launch_bounds__(kThreads)
 prefill_generic_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
                          const float* __restrict__ part, T* __restrict__ y, int BH, int n, int dk, int dv,
-                         int P, int C, int nslices, int seg0, int seg_len) {
+                         int P, int C, int nslices, int seg0, int seg_len, int qg) {
   extern __shared__ float lds[];
   const int E = dv + 1;
   float* xq = lds;                 // [C][dk]
@@ -673,7 +675,7 @@ prefill_generic_finalize(const T* __restrict__ q, const T* __restrict__ k, const
   const int cn = min(C, n - t0);
   const int tid = threadIdx.x;
   const float scale = 1.0f / sqrtf((float)dk);
-  load_chunk(q, k, v, bh, n, t0, cn, C, dk, dv, xq, xk, ve);
+  load_chunk(q, k, v, bh, n, t0, cn, C, dk, dv, xq, xk, ve, qg);
   __syncthreads();
   for (int rb = 0; rb < cn; rb += kFinRows) {
     const int rn = min(kFinRows, cn - rb);
@@ -704,7 +706,7 @@ prefill_generic_finalize(const T* __restrict__ q, const T* __restrict__ k, const
     for (int o = tid; o < rn * dv; o += kThreads) {
       const int r = o / dv;
       const int j = o - r * dv;
-      y[(bh * n + t0 + rb + r) * (int64_t)dv + j] = from_f32<T>(O[r * E + j] / O[r * E + dv]);
+      y[(bh * qg * n + t0 + rb + r) * (int64_t)dv + j] = from_f32<T>(O[r * E + j] / O[r * E + dv]);
     }
     __syncthreads();
   }
@@ -947,7 +949,7 @@ bool plan_prefill_generic(int64_t D, int BH, int n, int dk, int dv, int chunk, s
 hipError_t launch_prefill_generic(const void* q, const void* k, const void* v, void* y, bool bf16, int BH,
                                   int n, int dk, int dv, int chunk, const DevTable& t,
                                   const PrefillGenericPlan& plan, float* S_state, float* partial,
-                                  hipStream_t s) {
+                                  hipStream_t s, int qg) {
   const int C = chunk;
   hipError_t ea;
   if (bf16) {
@@ -970,11 +972,11 @@ hipError_t launch_prefill_generic(const void* q, const void* k, const void* v, v
     if (bf16)
       hipLaunchKernelGGL(prefill_generic_main<bf16_t>, g1, dim3(kThreads), plan.lds_main, s,
                          (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, t.packed, t.weight, t.D,
-                         S_state, partial, BH, n, dk, dv, C, plan.fs, seg0, plan.seg_len, first);
+                         S_state, partial, BH, n, dk, dv, C, plan.fs, seg0, plan.seg_len, first, qg);
     else
       hipLaunchKernelGGL(prefill_generic_main<float>, g1, dim3(kThreads), plan.lds_main, s,
                          (const float*)q, (const float*)k, (const float*)v, t.packed, t.weight, t.D, S_state,
-                         partial, BH, n, dk, dv, C, plan.fs, seg0, plan.seg_len, first);
+                         partial, BH, n, dk, dv, C, plan.fs, seg0, plan.seg_len, first, qg);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int seg_tokens = std::min(plan.seg_len, n - seg0);
@@ -982,11 +984,11 @@ hipError_t launch_prefill_generic(const void* q, const void* k, const void* v, v
     if (bf16)
       hipLaunchKernelGGL(prefill_generic_finalize<bf16_t>, g2, dim3(kThreads), plan.lds_final, s,
                          (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, partial, (bf16_t*)y, BH, n,
-                         dk, dv, t.P, C, plan.nslices, seg0, plan.seg_len);
+                         dk, dv, t.P, C, plan.nslices, seg0, plan.seg_len, qg);
     else
       hipLaunchKernelGGL(prefill_generic_finalize<float>, g2, dim3(kThreads), plan.lds_final, s,
                          (const float*)q, (const float*)k, (const float*)v, partial, (float*)y, BH, n, dk,
-                         dv, t.P, C, plan.nslices, seg0, plan.seg_len);
+                         dv, t.P, C, plan.nslices, seg0, plan.seg_len, qg);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

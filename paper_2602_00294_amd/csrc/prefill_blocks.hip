@@ -268,7 +268,8 @@ __global__ void __launch_bounds__(NW * 64)
 prefill_blocks_main(const u16* __restrict__ q, const u16* __restrict__ k, const u16* __restrict__ v,
                   const uint2* __restrict__ pmeta, const int* __restrict__ slice_ng,
                   const uint32_t* __restrict__ colmeta_g, const int* __restrict__ zmap,
-                  float* __restrict__ partial, float* __restrict__ S_out, int BH, int n, int C, int nslices) {
+                  float* __restrict__ partial, float* __restrict__ S_out, int BH, int n, int C, int nslices,
+                  int qg) {
   static_assert(DK == DV, "matrix-core path assumes d_k == d_v");
   using G = Geo<DK>;
   using L = MainLds<DK, DV, NW, PPW>;
@@ -335,7 +336,7 @@ prefill_blocks_main(const u16* __restrict__ q, const u16* __restrict__ k, const 
 
   const int G_tok = C < kGroup ? C : kGroup;  // tokens per group
   const int ngroups = C / G_tok;
-  const u16* qh = q + bh * (int64_t)n * DK;
+  const u16* qh = q + bh * (int64_t)qg * n * DK;  // qg query heads per key/value head
   const u16* kh = k + bh * (int64_t)n * DK;
   const u16* vh = v + bh * (int64_t)n * DV;
 
@@ -634,7 +635,7 @@ template <int DK, int DV>
 __global__ void __launch_bounds__(256)
 prefill_blocks_finalize(const u16* __restrict__ q, const u16* __restrict__ k, const u16* __restrict__ v,
                       const float* __restrict__ partial, u16* __restrict__ y, int BH, int n, int C, int nslices,
-                      int P) {
+                      int P, int qg) {
   constexpr int E = DV + 1;
   constexpr int NT = DV / 16;
   const FinLayout L(DK, DV, C);
@@ -662,7 +663,7 @@ prefill_blocks_finalize(const u16* __restrict__ q, const u16* __restrict__ k, co
     const int c8 = (i - tok * (DK / 8)) * 8;
     uint4 qv = {0u, 0u, 0u, 0u}, kv = {0u, 0u, 0u, 0u};
     if (tok < cn) {
-      qv = *(const uint4*)(q + (bh * n + t0 + tok) * DK + c8);
+      qv = *(const uint4*)(q + (bh * qg * n + t0 + tok) * DK + c8);
       kv = *(const uint4*)(k + (bh * n + t0 + tok) * DK + c8);
     }
     *(uint4*)(Qs + tok * L.qs + c8 * 2) = qv;
@@ -744,7 +745,7 @@ prefill_blocks_finalize(const u16* __restrict__ q, const u16* __restrict__ k, co
       if (qi < cn) {
         float o = acc[i];
         for (int s = 0; s < nslices; ++s) o += partial[(((int64_t)s * BH + bh) * n + t0 + qi) * E + col];
-        y[(bh * n + t0 + qi) * DV + col] = f32_to_bf16(o / Zs[qi]).bits;
+        y[(bh * qg * n + t0 + qi) * DV + col] = f32_to_bf16(o / Zs[qi]).bits;
       }
     }
   }
@@ -957,20 +958,20 @@ int host_nslices(int d) {
 
 template <int DK, int DV, int PPW>
 hipError_t launch_typed(const u16* q, const u16* k, const u16* v, u16* y, float* S_out, int BH, int n, int C,
-                        const DeviceTables& dt, float* partial, hipStream_t s) {
+                        const DeviceTables& dt, float* partial, hipStream_t s, int qg) {
   using L = MainLds<DK, DV, kNW, PPW>;
   auto kmain = prefill_blocks_main<DK, DV, kNW, PPW>;
   hipError_t e = hipFuncSetAttribute((const void*)kmain, hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kmain, dim3((unsigned)dt.nslices, (unsigned)BH), dim3(kNW * 64), L::kBytes, s, q, k, v,
-                     dt.pairs, dt.slice_ng, dt.colmeta, dt.zmap, partial, S_out, BH, n, C, dt.nslices);
+                     dt.pairs, dt.slice_ng, dt.colmeta, dt.zmap, partial, S_out, BH, n, C, dt.nslices, qg);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const FinLayout F(DK, DV, C);
   auto kfin = prefill_blocks_finalize<DK, DV>;
   e = hipFuncSetAttribute((const void*)kfin, hipFuncAttributeMaxDynamicSharedMemorySize, F.bytes);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kfin, dim3((unsigned)((n + C - 1) / C), (unsigned)BH), dim3(256), (size_t)F.bytes, s, q, k,
-                     v, partial, y, BH, n, C, dt.nslices, 4);
+                     v, partial, y, BH, n, C, dt.nslices, 4, qg);
   return hipGetLastError();
 }
 
@@ -990,7 +991,7 @@ bool plan_prefill_blocks(int BH, int n, int dk, int dv, int P, int chunk, MfmaPr
 
 hipError_t launch_prefill_blocks(const void* q, const void* k, const void* v, void* y, float* S_out, int BH,
                                int n, int dk, int dv, int P, int chunk, const MfmaPrefillPlan& plan,
-                               void* workspace, hipStream_t s) {
+                               void* workspace, hipStream_t s, int qg) {
   (void)P;
   (void)dv;
   DeviceTables dt;
@@ -1000,8 +1001,8 @@ hipError_t launch_prefill_blocks(const void* q, const void* k, const void* v, vo
   const u16* qq = (const u16*)q;
   const u16* kk = (const u16*)k;
   const u16* vv = (const u16*)v;
-  if (dk == 32) return launch_typed<32, 32, 8>(qq, kk, vv, (u16*)y, S_out, BH, n, chunk, dt, partial, s);
-  return launch_typed<16, 16, 16>(qq, kk, vv, (u16*)y, S_out, BH, n, chunk, dt, partial, s);
+  if (dk == 32) return launch_typed<32, 32, 8>(qq, kk, vv, (u16*)y, S_out, BH, n, chunk, dt, partial, s, qg);
+  return launch_typed<16, 16, 16>(qq, kk, vv, (u16*)y, S_out, BH, n, chunk, dt, partial, s, qg);
 }
 
 }  // namespace sata

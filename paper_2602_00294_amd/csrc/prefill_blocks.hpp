@@ -14,6 +14,6 @@ bool plan_prefill_blocks(int BH, int n, int dk, int dv, int P, int chunk, MfmaPr
 
 hipError_t launch_prefill_blocks(const void* q, const void* k, const void* v, void* y, float* S_out, int BH,
                                  int n, int dk, int dv, int P, int chunk, const MfmaPrefillPlan& plan,
-                                 void* workspace, hipStream_t s);
+                                 void* workspace, hipStream_t s, int qg = 1);
 
 }  // namespace sata

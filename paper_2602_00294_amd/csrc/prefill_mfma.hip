@@ -268,7 +268,7 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
                   const int4* __restrict__ slices, const uint32_t* __restrict__ slots,
                   const float* __restrict__ facs, const int* __restrict__ prep_idx,
                   const float* __restrict__ prep_scale, const int* __restrict__ low_idx,
-                  float* __restrict__ partial, float* __restrict__ S_out, int BH, int n, int nslices) {
+                  float* __restrict__ partial, float* __restrict__ S_out, int BH, int n, int nslices, int qg) {
   constexpr int DV = DK;
   static_assert(DK == 32, "value columns must fill the 32-row MFMA tile");
   constexpr int E = DV + 1;
@@ -307,7 +307,7 @@ prefill_mfma_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
   for (int p = 0; p < PPW; ++p)
     meta[p] = __builtin_amdgcn_readfirstlane(slots[((int64_t)slice * kNW + wave) * PPW + p]);
 
-  const u16* qh_ = q + bh * (int64_t)n * DK;
+  const u16* qh_ = q + bh * (int64_t)qg * n * DK;  // qg query heads per key/value head
   const u16* kh_ = k + bh * (int64_t)n * DK;
   const u16* vh_ = v + bh * (int64_t)n * DV;
   const int nch = (n + kC - 1) / kC;
@@ -838,7 +838,7 @@ template <int DK, int DV>
 __global__ void __launch_bounds__(256, 8)
 prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, const u16* __restrict__ v,
                       const float* __restrict__ partial, u16* __restrict__ y, int BH, int n, int C, int nslices,
-                      int P, int PS) {
+                      int P, int PS, int qg) {
   constexpr int E = DV + 1;
   constexpr int NT = DV / 16;
   const FinLayout L(DK, DV, C);
@@ -895,7 +895,7 @@ prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, cons
     const int c8 = (i - tok * (DK / 8)) * 8;
     uint4 qv = {0u, 0u, 0u, 0u}, kv = {0u, 0u, 0u, 0u};
     if (tok < cn) {
-      qv = *(const uint4*)(q + (bh * n + t0 + tok) * DK + c8);
+      qv = *(const uint4*)(q + (bh * qg * n + t0 + tok) * DK + c8);
       kv = *(const uint4*)(k + (bh * n + t0 + tok) * DK + c8);
     }
     *(uint4*)(Qs + tok * L.qs + c8 * 2) = qv;
@@ -992,7 +992,7 @@ prefill_mfma_finalize(const u16* __restrict__ q, const u16* __restrict__ k, cons
       uint2 w;
       w.x = (uint32_t)f32_to_bf16((acc[0] + pre[it].x) / z).bits | ((uint32_t)f32_to_bf16((acc[1] + pre[it].y) / z).bits << 16);
       w.y = (uint32_t)f32_to_bf16((acc[2] + pre[it].z) / z).bits | ((uint32_t)f32_to_bf16((acc[3] + pre[it].w) / z).bits << 16);
-      *(uint2*)(y + (bh * n + t0 + qi) * DV + 16 * j + 4 * g4) = w;
+      *(uint2*)(y + (bh * qg * n + t0 + qi) * DV + 16 * j + 4 * g4) = w;
     }
   }
 }
@@ -1333,21 +1333,21 @@ hipError_t get_tables(int d, hipStream_t s, DeviceTables* out) {
 
 template <int DK>
 hipError_t launch_typed(const u16* q, const u16* k, const u16* v, u16* y, float* S_out, int BH, int n,
-                        const DeviceTables& dt, float* partial, hipStream_t s) {
+                        const DeviceTables& dt, float* partial, hipStream_t s, int qg) {
   using L = Lds<DK>;
   auto kmain = prefill_mfma_main<DK, Ppw<DK>::value>;
   hipError_t e = hipFuncSetAttribute((const void*)kmain, hipFuncAttributeMaxDynamicSharedMemorySize, L::BYTES);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kmain, dim3((unsigned)dt.nslices * (unsigned)BH), dim3(kNW * 64), L::BYTES, s, q, k, v,
                      dt.slices, dt.slots, dt.facs, dt.prep_idx, dt.prep_scale, dt.low_idx, partial, S_out, BH, n,
-                     dt.nslices);
+                     dt.nslices, qg);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const FinLayout F(DK, DK, kC);
   auto kfin = prefill_mfma_finalize<DK, DK>;
   e = hipFuncSetAttribute((const void*)kfin, hipFuncAttributeMaxDynamicSharedMemorySize, F.bytes);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kfin, dim3((unsigned)((n + kC - 1) / kC), (unsigned)BH), dim3(256), (size_t)F.bytes, s, q, k,
-                     v, partial, y, BH, n, kC, dt.nslices, 4, kPS);
+                     v, partial, y, BH, n, kC, dt.nslices, 4, kPS, qg);
   return hipGetLastError();
 }
 
@@ -1369,7 +1369,7 @@ bool plan_prefill_mfma(int BH, int n, int dk, int dv, int P, int chunk, MfmaPref
 
 hipError_t launch_prefill_mfma(const void* q, const void* k, const void* v, void* y, float* S_out, int BH,
                                int n, int dk, int dv, int P, int chunk, const MfmaPrefillPlan& plan,
-                               void* workspace, hipStream_t s) {
+                               void* workspace, hipStream_t s, int qg) {
   (void)P;
   (void)dv;
   (void)chunk;
@@ -1381,7 +1381,7 @@ hipError_t launch_prefill_mfma(const void* q, const void* k, const void* v, void
   const u16* qq = (const u16*)q;
   const u16* kk = (const u16*)k;
   const u16* vv = (const u16*)v;
-  return launch_typed<32>(qq, kk, vv, (u16*)y, S_out, BH, n, dt, partial, s);
+  return launch_typed<32>(qq, kk, vv, (u16*)y, S_out, BH, n, dt, partial, s, qg);
 }
 
 }  // namespace sata

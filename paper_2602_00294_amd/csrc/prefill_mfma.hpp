@@ -19,6 +19,6 @@ bool plan_prefill_mfma(int BH, int n, int dk, int dv, int P, int chunk, MfmaPref
 
 hipError_t launch_prefill_mfma(const void* q, const void* k, const void* v, void* y, float* S_out, int BH,
                                int n, int dk, int dv, int P, int chunk, const MfmaPrefillPlan& plan,
-                               void* workspace, hipStream_t s);
+                               void* workspace, hipStream_t s, int qg = 1);
 
 }  // namespace sata

@@ -259,6 +259,55 @@ PrefillPath prefill_path(sata_dtype dt, int BH, int n, int d_k, int d_v, int P, 
   return PrefillPath::kFloat32;
 }
 
+// One prefill over BH key/value heads; q and y hold qg query heads per
+// key/value head (head bh's queries start at head bh * qg of q).
+sata_status prefill_dispatch(const void* q, const void* k, const void* v, sata_dtype dt, int BH, int n, int d_k,
+                             int d_v, int P, int chunk, void* y, float* S_out, hipStream_t s, int64_t D, int qg) {
+  const int E = d_v + 1;
+  hipError_t e;
+  sata_status st;
+  if (n == 0) {
+    if (S_out) {
+      if ((e = sata::launch_fill_zero(S_out, (int64_t)BH * D * E, s)) != hipSuccess)
+        return hip_fail(e, "fill launch");
+    }
+    return ok();
+  }
+  sata::DevTable t;
+  if ((st = get_table(d_k, P, s, &t)) != SATA_OK) return st;
+
+  // bf16 fast path on the matrix cores where a tuned kernel exists
+  sata::MfmaPrefillPlan mp;
+  const PrefillPath path = prefill_path(dt, BH, n, d_k, d_v, P, chunk);
+  if (path == PrefillPath::kMfma32 && sata::plan_prefill_mfma(BH, n, d_k, d_v, P, chunk, &mp)) {
+    void* ws = nullptr;
+    if ((st = get_workspace(mp.workspace_bytes, s, &ws)) != SATA_OK) return st;
+    e = sata::launch_prefill_mfma(q, k, v, y, S_out, BH, n, d_k, d_v, P, chunk, mp, ws, s, qg);
+    if (e != hipSuccess) return hip_fail(e, "prefill (matrix-core) launch");
+    return ok();
+  }
+  if (path == PrefillPath::kBlocks && sata::plan_prefill_blocks(BH, n, d_k, d_v, P, chunk, &mp)) {
+    void* ws = nullptr;
+    if ((st = get_workspace(mp.workspace_bytes, s, &ws)) != SATA_OK) return st;
+    e = sata::launch_prefill_blocks(q, k, v, y, S_out, BH, n, d_k, d_v, P, chunk, mp, ws, s, qg);
+    if (e != hipSuccess) return hip_fail(e, "prefill (matrix-core, per-block) launch");
+    return ok();
+  }
+
+  sata::PrefillGenericPlan plan;
+  if (!sata::plan_prefill_generic(D, BH, n, d_k, d_v, chunk, kMaxWorkspace, &plan))
+    return fail(SATA_ERR_UNSUPPORTED, "no slice size fits on chip for d_k=%d d_v=%d chunk=%d", d_k, d_v, chunk);
+  const size_t state_bytes = S_out ? 0 : sizeof(float) * (size_t)BH * D * E;
+  void* ws = nullptr;
+  if ((st = get_workspace(plan.partial_bytes + state_bytes, s, &ws)) != SATA_OK) return st;
+  float* partial = (float*)ws;
+  float* S_state = S_out ? S_out : (float*)((char*)ws + plan.partial_bytes);
+  e = sata::launch_prefill_generic(q, k, v, y, dt == SATA_BF16, BH, n, d_k, d_v, chunk, t, plan, S_state,
+                                   partial, s, qg);
+  if (e != hipSuccess) return hip_fail(e, "prefill launch");
+  return ok();
+}
+
 sata_status decode_step(float* S, float* R, const void* q, const void* k, const void* v, sata_dtype dt, int B,
                         int H, int d_k, int d_v, int P, void* y, void* stream) {
   if (!valid_dtype(dt)) return fail(SATA_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
@@ -372,49 +421,31 @@ sata_status sata_prefill(const void* q, const void* k, const void* v, sata_dtype
   sata_status st = check_prefill_args(dt, B, H, n, d_k, d_v, P, chunk, &D);
   if (st != SATA_OK) return st;
   if (n > 0 && (!q || !k || !v || !y)) return fail(SATA_ERR_INVALID_ARG, "null tensor pointer");
-  const int BH = B * H;
-  const int E = d_v + 1;
-  hipStream_t s = (hipStream_t)stream;
-  hipError_t e;
-  if (n == 0) {
-    if (S_out) {
-      if ((e = sata::launch_fill_zero(S_out, (int64_t)BH * D * E, s)) != hipSuccess)
-        return hip_fail(e, "fill launch");
-    }
-    return ok();
-  }
-  sata::DevTable t;
-  if ((st = get_table(d_k, P, s, &t)) != SATA_OK) return st;
+  return prefill_dispatch(q, k, v, dt, B * H, n, d_k, d_v, P, chunk, y, S_out, (hipStream_t)stream, D, 1);
+}
 
-  // bf16 fast path on the matrix cores where a tuned kernel exists
-  sata::MfmaPrefillPlan mp;
-  const PrefillPath path = prefill_path(dt, BH, n, d_k, d_v, P, chunk);
-  if (path == PrefillPath::kMfma32 && sata::plan_prefill_mfma(BH, n, d_k, d_v, P, chunk, &mp)) {
-    void* ws = nullptr;
-    if ((st = get_workspace(mp.workspace_bytes, s, &ws)) != SATA_OK) return st;
-    e = sata::launch_prefill_mfma(q, k, v, y, S_out, BH, n, d_k, d_v, P, chunk, mp, ws, s);
-    if (e != hipSuccess) return hip_fail(e, "prefill (matrix-core) launch");
-    return ok();
+sata_status sata_prefill_grouped(const void* q, const void* k, const void* v, sata_dtype dt, int B, int H_kv,
+                                 int G, int n, int d_k, int d_v, int P, int chunk, void* y, float* S_out,
+                                 void* stream) {
+  if (G < 1) return fail(SATA_ERR_INVALID_ARG, "G=%d must be >= 1", G);
+  if (B >= 1 && H_kv >= 1 && (int64_t)B * H_kv * G > kMaxHeads)
+    return fail(SATA_ERR_TOO_LARGE, "B*H_kv*G=%lld exceeds %d", (long long)B * H_kv * G, kMaxHeads);
+  int64_t D = 0;
+  sata_status st = check_prefill_args(dt, B, H_kv, n, d_k, d_v, P, chunk, &D);
+  if (st != SATA_OK) return st;
+  if (n > 0 && (!q || !k || !v || !y)) return fail(SATA_ERR_INVALID_ARG, "null tensor pointer");
+  const size_t esz = dt == SATA_BF16 ? 2 : 4;
+  // query head g + G h of each batch row is member g of key/value head h's
+  // group: with the heads of the call numbered by key/value head, member g's
+  // queries and outputs start g heads in and lie G heads apart
+  for (int g = 0; g < G; ++g) {
+    const void* qg = (const char*)q + esz * (size_t)g * (size_t)n * (size_t)d_k;
+    void* yg = (char*)y + esz * (size_t)g * (size_t)n * (size_t)d_v;
+    st = prefill_dispatch(qg, k, v, dt, B * H_kv, n, d_k, d_v, P, chunk, yg, g == 0 ? S_out : nullptr,
+                          (hipStream_t)stream, D, G);
+    if (st != SATA_OK) return st;
+    if (n == 0) break;
   }
-  if (path == PrefillPath::kBlocks && sata::plan_prefill_blocks(BH, n, d_k, d_v, P, chunk, &mp)) {
-    void* ws = nullptr;
-    if ((st = get_workspace(mp.workspace_bytes, s, &ws)) != SATA_OK) return st;
-    e = sata::launch_prefill_blocks(q, k, v, y, S_out, BH, n, d_k, d_v, P, chunk, mp, ws, s);
-    if (e != hipSuccess) return hip_fail(e, "prefill (matrix-core, per-block) launch");
-    return ok();
-  }
-
-  sata::PrefillGenericPlan plan;
-  if (!sata::plan_prefill_generic(D, BH, n, d_k, d_v, chunk, kMaxWorkspace, &plan))
-    return fail(SATA_ERR_UNSUPPORTED, "no slice size fits on chip for d_k=%d d_v=%d chunk=%d", d_k, d_v, chunk);
-  const size_t state_bytes = S_out ? 0 : sizeof(float) * (size_t)BH * D * E;
-  void* ws = nullptr;
-  if ((st = get_workspace(plan.partial_bytes + state_bytes, s, &ws)) != SATA_OK) return st;
-  float* partial = (float*)ws;
-  float* S_state = S_out ? S_out : (float*)((char*)ws + plan.partial_bytes);
-  e = sata::launch_prefill_generic(q, k, v, y, dt == SATA_BF16, BH, n, d_k, d_v, chunk, t, plan, S_state,
-                                   partial, s);
-  if (e != hipSuccess) return hip_fail(e, "prefill launch");
   return ok();
 }
 

@@ -107,6 +107,16 @@ def test_decode_and_feature_map_validation(lib):
     assert lib.sata_feature_map(NULL, 0, 3, 4, 3, FAKE, NULL) == -1
 
 
+def test_prefill_grouped_validation(lib):
+    # (q, k, v, dtype, B, H_kv, G, n, d_k, d_v, P, chunk, y, S_out, stream)
+    g = lib.sata_prefill_grouped
+    assert g(FAKE, FAKE, FAKE, 0, 1, 1, 0, 8, 4, 4, 4, 64, FAKE, NULL, NULL) == -1      # G = 0
+    assert g(FAKE, FAKE, FAKE, 0, 1, 4096, 16, 8, 4, 4, 4, 64, FAKE, NULL, NULL) == -3  # B*H_kv*G = 65536
+    assert g(FAKE, FAKE, FAKE, 0, 1, 1, 2, 8, 4, 4, 4, 48, FAKE, NULL, NULL) == -2      # chunk
+    assert g(NULL, FAKE, FAKE, 0, 1, 1, 2, 8, 4, 4, 4, 64, FAKE, NULL, NULL) == -1      # null q
+    assert g(FAKE, FAKE, FAKE, 5, 1, 1, 2, 8, 4, 4, 4, 64, FAKE, NULL, NULL) == -1      # dtype
+
+
 def test_status_strings(lib):
     for code in (0, -1, -2, -3, -4):
         assert lib.sata_status_string(code)

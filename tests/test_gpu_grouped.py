@@ -91,3 +91,46 @@ def test_grouped_decode_deterministic_and_g1_is_decode_step(sata):
     yb = sata.decode_step(S4, q1, step[1], step[2], P)
     torch.cuda.synchronize()
     assert torch.equal(ya, yb) and torch.equal(S3, S4)
+
+
+@pytest.mark.parametrize("B,Hkv,G,n,d,P,chunk,dtype", [
+    (1, 2, 4, 150, 32, 4, 64, "bf16"),   # the d = 32 matrix-core kernel
+    (2, 2, 2, 97, 16, 4, 32, "bf16"),    # the per-block matrix-core kernel
+    (1, 3, 2, 70, 8, 4, 64, "f32"),      # the float32 kernel
+    (1, 1, 8, 40, 5, 3, 16, "f32"),
+])
+def test_grouped_prefill_matches_oracle(sata, B, Hkv, G, n, d, P, chunk, dtype):
+    """Every query head's rows against the oracle applied to its own queries and
+    its key/value head's tokens; each member of a group bitwise equal to the
+    single-head prefill of its queries; the states equal to the plain prefill's
+    (they depend on the keys and values only); then a grouped decode step."""
+    _say(f"grouped prefill B={B} H_kv={Hkv} G={G} n={n} d={d} P={P} chunk={chunk} {dtype}")
+    q, k, v = _inputs(140 + d, B, Hkv, G, n + 1, d, dtype)
+    dev = lambda a: to_dev(np.ascontiguousarray(a), dtype)
+    qd, kd, vd = dev(q[:, :, :n]), dev(k[:, :, :n]), dev(v[:, :, :n])
+    y, S = sata.prefill_grouped(qd, kd, vd, P, chunk)
+    torch.cuda.synchronize()
+    ops = operands(sata, dtype, B, Hkv, n, d, d, P, chunk)
+    yh = to_host(y)
+    for b in range(B):
+        for hq in range(Hkv * G):
+            h = hq // G
+            yr, _, kap = oracle.taylor_attention(q[b, hq, :n], k[b, h, :n], v[b, h, :n], P)
+            check_rows(yh[b, hq], yr, kap, y_tol(ops, dtype), P, f"b{b} query head {hq}")
+    for g in range(G):
+        yg, Sg = sata.prefill(qd[:, g::G].contiguous(), kd, vd, P, chunk)
+        torch.cuda.synchronize()
+        assert torch.equal(yg, y[:, g::G]), f"member {g}"
+        assert torch.equal(Sg, S)
+    for b in range(B):
+        for h in range(Hkv):
+            check_state(to_host(S[b, h]), k[b, h, :n], v[b, h, :n], P, ops, n, chunk, f"state b{b} h{h}")
+    yd = to_host(sata.decode_step_grouped(S, dev(q[:, :, n]), dev(k[:, :, n]), dev(v[:, :, n]), P)) \
+        if S.data_ptr() % 16 == 0 else None
+    torch.cuda.synchronize()
+    if yd is not None:
+        for b in range(B):
+            for hq in range(Hkv * G):
+                h = hq // G
+                yr, _, kap = oracle.taylor_attention_rows(q[b, hq], k[b, h], v[b, h], P, [n])
+                check_rows(yd[b, hq][None], yr, kap, y_tol(ops, dtype), P, f"decode b{b} query head {hq}")
