@@ -38,6 +38,12 @@ What is computed (sections of the paper in brackets):
                         |[v_t, 1]|: the size of the terms that make up each
                         state entry, against which a rounded state is judged
                         [App. A2, accumulated feature states].
+* ``taylor_attention_backward``
+                        the gradients dL/dq, dL/dk, dL/dv of a loss through
+                        the causal output, for a given dL/dy: the derivative
+                        of the direct definition above, written out row by row
+                        (the paper names training as the next step and gives
+                        no backward; this is calculus on App. A2's output).
 * ``feature_count`` / ``state_elems`` / ``flops_per_token``
                         the closed forms of Sec. 2.6 and Sec. 2.7.
 
@@ -68,7 +74,7 @@ from typing import Iterable, List, Sequence, Tuple
 import numpy as np
 
 __all__ = [
-    "taylor_poly", "taylor_attention", "taylor_attention_rows", "softmax_attention",
+    "taylor_poly", "taylor_attention", "taylor_attention_rows", "taylor_attention_backward", "softmax_attention",
     "softmax_attention_rows", "multi_indices", "multiplicity", "alpha", "feature_weights",
     "phi_ref", "state_ref", "state_abs_ref", "readout_ref", "recurrent_attention", "decode_ref",
     "feature_count", "degree_count", "state_elems", "flops_per_token",
@@ -186,6 +192,44 @@ def taylor_attention_rows(q, k, v, P: int, rows: Sequence[int]):
         Z[i] = den
         kappa[i] = np.abs(w).sum() / abs(den)
     return y, Z, kappa
+
+
+def taylor_attention_backward(q, k, v, dy, P: int, block: int = 512):
+    """Gradients of the causal truncated-Taylor attention of one head.
+
+    q, k: [n, d_k], v: [n, d_v], dy = dL/dy: [n, d_v].  With, for t <= T,
+        s_Tt = q_T . k_t / c,  w_Tt = f_P(s_Tt),  Z_T = sum_t w_Tt,
+        y_T  = sum_t w_Tt v_t / Z_T,
+    the chain rule gives
+        dL/dw_Tt = dy_T . (v_t - y_T) / Z_T
+        dL/ds_Tt = dL/dw_Tt * f_P'(s_Tt),  f_P' = f_{P-1}  (the series cut one term earlier)
+        dL/dq_T  = sum_{t <= T} dL/ds_Tt k_t / c
+        dL/dk_t  = sum_{T >= t} dL/ds_Tt q_T / c
+        dL/dv_t  = sum_{T >= t} w_Tt dy_T / Z_T.
+    Returns (dq [n, d_k], dk [n, d_k], dv [n, d_v]), float64."""
+    q, k, v, dy = _as64(q), _as64(k), _as64(v), _as64(dy)
+    n, d_k = q.shape
+    c = math.sqrt(d_k)
+    dq = np.zeros_like(q)
+    dk = np.zeros_like(k)
+    dv = np.zeros_like(v)
+    for r0 in range(0, n, block):
+        r1 = min(n, r0 + block)
+        s = (q[r0:r1] @ k[:r1].T) / c                       # [rows, r1]
+        rows = np.arange(r0, r1)[:, None]
+        cols = np.arange(r1)[None, :]
+        mask = cols <= rows                                  # inclusive causal mask
+        w = np.where(mask, taylor_poly(s, P), 0.0)
+        dw_ds = np.where(mask, taylor_poly(s, P - 1), 0.0)
+        Z = w.sum(axis=1)
+        y = (w @ v[:r1]) / Z[:, None]
+        g = dy[r0:r1] / Z[:, None]                           # dL/dN_T
+        dL_dw = g @ v[:r1].T - np.sum(g * y, axis=1, keepdims=True)
+        dL_ds = np.where(mask, dL_dw * dw_ds, 0.0)
+        dq[r0:r1] = (dL_ds @ k[:r1]) / c
+        dk[:r1] += (dL_ds.T @ q[r0:r1]) / c
+        dv[:r1] += w.T @ g
+    return dq, dk, dv
 
 
 def softmax_attention(q, k, v, block: int = 512) -> np.ndarray:
