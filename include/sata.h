@@ -122,6 +122,27 @@ sata_status sata_prefill_grouped(const void* q, const void* k, const void* v, sa
                                  int B, int H_kv, int G, int n, int d_k, int d_v, int P, int chunk,
                                  void* y, float* S_out, void* stream);
 
+/* Gradients of the causal prefill: given dL/dy for every output, writes
+ * dL/dq, dL/dk and dL/dv (training is the next step the paper names, Sec. 4;
+ * the derivative is that of the causal output of App. A2).  The chunked scans
+ * run over the same constant-size states as the forward: the forward scan
+ * with S_T = sum_{t<=T} phi(k_t) (x) [v_t, 1] gives
+ *     dL/dq_T = J_phi(q_T)^T S_T h_T,   h_T = [dy_T / Z_T, -(dy_T . y_T) / Z_T],
+ * and the reverse scan with U_t = sum_{T>=t} phi(q_T) (x) h_T gives
+ *     dL/dk_t = J_phi(k_t)^T U_t [v_t, 1],   dL/dv_t = (U_t^T phi(k_t))[0:d_v],
+ * J_phi being the Jacobian of the feature map; inside a chunk the gradient of
+ * f_P(q.k / sqrt(d_k)), f_{P-1}(s) k / sqrt(d_k), is used directly.
+ *   q, k  : [B][H][n][d_k], v, dy : [B][H][n][d_v], dtype dt (device)
+ *   dq, dk: [B][H][n][d_k], dv : [B][H][n][d_v], dtype dt (device, written)
+ * All arithmetic is float32 (the forward is recomputed, not passed in).
+ * chunk: 16, 32 or 64; d_k, d_v <= 64 (SATA_ERR_UNSUPPORTED otherwise).
+ * Workspace: float32 dL/d[N|Z] for every token (4 (d_v+1) bytes per
+ * head-token), one state, and per-segment partial sums of at most 512 MB.
+ * n = 0 writes nothing. */
+sata_status sata_backward(const void* q, const void* k, const void* v, const void* dy, sata_dtype dt,
+                          int B, int H, int n, int d_k, int d_v, int P, int chunk,
+                          void* dq, void* dk, void* dv, void* stream);
+
 /* Precision of the operands of the state contractions that sata_prefill uses
  * for these arguments (host only, no GPU use; same validation as sata_prefill):
  * *operands = SATA_BF16 when they run on the matrix cores with bfloat16

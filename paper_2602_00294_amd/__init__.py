@@ -7,8 +7,8 @@ libsata.so); this package is the thin Python binding over it.
     y, S = prefill(q, k, v, P=4, chunk=64)      # q, k, v: [B, H, n, d] on the GPU
     y_t = decode_step(S, q_t, k_t, v_t, P=4)     # S updated in place
 """
-from ._binding import (SataError, decode_step, decode_step_compensated, decode_step_grouped, feature_count, feature_index, feature_map, load_library,
+from ._binding import (SataError, backward, decode_step, decode_step_compensated, decode_step_grouped, feature_count, feature_index, feature_map, load_library,
                        prefill, prefill_grouped, prefill_operands, release, residual_elems, state_elems)
 
-__all__ = ["SataError", "decode_step", "decode_step_compensated", "decode_step_grouped", "feature_count", "feature_index", "feature_map", "load_library",
+__all__ = ["SataError", "backward", "decode_step", "decode_step_compensated", "decode_step_grouped", "feature_count", "feature_index", "feature_map", "load_library",
            "prefill", "prefill_grouped", "prefill_operands", "release", "residual_elems", "state_elems"]

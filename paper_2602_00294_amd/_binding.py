@@ -50,6 +50,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.sata_prefill.restype = i32
     lib.sata_prefill_grouped.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp]
     lib.sata_prefill_grouped.restype = i32
+    lib.sata_backward.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp]
+    lib.sata_backward.restype = i32
     lib.sata_prefill_operands.argtypes = [i32, i32, i32, i32, i32, i32, i32, i32, ctypes.POINTER(i32)]
     lib.sata_prefill_operands.restype = i32
     lib.sata_decode_step.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp]
@@ -262,6 +264,29 @@ def prefill_grouped(q, k, v, P: int, chunk: int = 64, want_state: bool = True, y
                                                    _ptr(y), _ptr(S) if S is not None else ctypes.c_void_p(None),
                                                    _stream_ptr()), "sata_prefill_grouped")
     return y, S
+
+
+def backward(q, k, v, dy, P: int, chunk: int = 64):
+    """Gradients of the causal prefill's output y for dL/dy = dy.
+    q, k: [B, H, n, d_k]; v, dy: [B, H, n, d_v].  Returns (dq, dk, dv) in q's dtype."""
+    torch = _torch()
+    code = _dtype_code(q)
+    _check_same_dtype(q, k=k, v=v, dy=dy)
+    if q.dim() != 4 or v.dim() != 4:
+        raise ValueError("q, k, v, dy must be [B, H, n, d]")
+    B, H, n, dk = q.shape
+    dv = v.shape[-1]
+    _check_shape(k, "k", (B, H, n, dk))
+    _check_shape(v, "v", (B, H, n, dv))
+    _check_shape(dy, "dy", (B, H, n, dv))
+    _features(dk, P)
+    for name, t in (("q", q), ("k", k), ("v", v), ("dy", dy)):
+        _check_tensor(t, name, q.device)
+    dq, dkk, dvv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    with torch.cuda.device(q.device):
+        _check(load_library().sata_backward(_ptr(q), _ptr(k), _ptr(v), _ptr(dy), code, B, H, n, dk, dv, P, chunk,
+                                            _ptr(dq), _ptr(dkk), _ptr(dvv), _stream_ptr()), "sata_backward")
+    return dq, dkk, dvv
 
 
 def decode_step(S, q, k, v, P: int, y=None):

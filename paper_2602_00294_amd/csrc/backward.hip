@@ -1,0 +1,562 @@
+// Backward pass of causal symmetry-aware Taylor attention: dL/dq, dL/dk and
+// dL/dv for a given dL/dy, as chunked scans over the same constant-size states
+// as the forward (App. A2), in float32 for both input dtypes.
+//
+// With o_T = phi(q_T)^T S_T = [N_T | Z_T] (S_T = sum_{t<=T} phi(k_t) (x) [v_t|1]),
+// y_T = N_T / Z_T and g_T = dL/dy_T, the loss sees o_T through
+//     h_T = dL/do_T = [g_T / Z_T | -(g_T . y_T) / Z_T]          (d_v + 1 values)
+// and the chain rule through the linear-attention form gives
+//     dL/dq_T = J_phi(q_T)^T (S_T h_T)                          (forward scan)
+//     dL/dk_t = J_phi(k_t)^T (U_t [v_t|1]),  dL/dv_t = (U_t^T phi(k_t))[0:d_v]
+//     with U_t = sum_{T>=t} phi(q_T) (x) h_T                     (reverse scan)
+// where J_phi is the Jacobian of the feature map.  In chunks of C tokens the
+// states before (S) or after (U) the chunk give the inter-chunk parts; inside
+// a chunk phi(q).phi(k) = f_P(s) and its gradient f_P'(s) k / sqrt(d_k) =
+// f_{P-1}(s) k / sqrt(d_k) give the intra-chunk parts directly.
+//
+// Passes, each over sequence segments whose partial sums fit the workspace:
+//   1. the forward readout (the float32 prefill's main kernel) and
+//      backward_h_finalize, which forms h_T;
+//   2. backward_dq_main: each workgroup keeps one feature slice of S in LDS,
+//      per chunk reads it out against h (u = S h) and applies the Jacobian of
+//      its features at q, then adds the chunk's keys; backward_dq_finalize adds
+//      the slices' partial gradients (in slice order) and the intra-chunk part;
+//   3. backward_dkv_main: the reverse scan with U; backward_dkv_finalize.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <type_traits>
+
+#include "device_common.hpp"
+#include "kernels.hpp"
+#include "table.hpp"
+
+namespace sata {
+
+namespace {
+
+constexpr int kBwThreads = 256;
+
+// Rows of q, k, [v | 1] and h of one chunk into LDS (zero beyond the sequence).
+template <typename T>
+__device__ void bw_load_chunk(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+                              const float* __restrict__ h, int64_t bh, int n, int t0, int cn, int C, int dk, int dv,
+                              float* xq, float* xk, float* ve, float* hh) {
+  const int E = dv + 1;
+  const int64_t off = (bh * n + t0) * (int64_t)dk;
+  for (int i = threadIdx.x; i < C * dk; i += kBwThreads) {
+    const int t = i / dk;
+    xq[i] = t < cn ? to_f32(q[off + i]) : 0.0f;
+    xk[i] = t < cn ? to_f32(k[off + i]) : 0.0f;
+  }
+  const int64_t voff = (bh * n + t0) * (int64_t)dv;
+  const int64_t hoff = (bh * n + t0) * (int64_t)E;
+  for (int i = threadIdx.x; i < C * E; i += kBwThreads) {
+    const int t = i / E;
+    const int j = i - t * E;
+    float val = 0.0f, hv = 0.0f;
+    if (t < cn) {
+      val = (j < dv) ? to_f32(v[voff + (int64_t)t * dv + j]) : 1.0f;
+      hv = h[hoff + i];
+    }
+    ve[i] = val;
+    hh[i] = hv;
+  }
+}
+
+// acc[a] += u * d phi_f(x) / d x[a] for one feature (packed multi-index pk,
+// weight w): phi_f = w prod_j x[i_j], so the derivative along x[i_j] of each
+// factor is w times the product of the other factors (prefix times suffix).
+__device__ __forceinline__ void add_feature_gradient(uint64_t pk, float w, float u, const float* x, float* acc) {
+  const int p = (int)(pk >> 56);
+  if (p == 0) return;
+  float xs[kMaxP];
+  int ix[kMaxP];
+#pragma unroll
+  for (int j = 0; j < kMaxP - 1; ++j) {
+    ix[j] = (int)((pk >> (8 * j)) & 0xff);
+    xs[j] = (j < p) ? x[ix[j]] : 1.0f;
+  }
+  float suf[kMaxP];
+  suf[kMaxP - 1] = 1.0f;
+#pragma unroll
+  for (int j = kMaxP - 2; j >= 0; --j) suf[j] = suf[j + 1] * xs[j];
+  float pre = w * u;
+#pragma unroll
+  for (int j = 0; j < kMaxP - 1; ++j) {
+    if (j < p) {
+      acc[ix[j]] += pre * suf[j + 1];
+      pre *= xs[j];
+    }
+  }
+}
+
+// Shared LDS layout of the two scan kernels (in floats; the 8-byte table
+// entries first, so they stay aligned):
+//   tpk [FS] (u64) | tw [FS] | Sl [FS][E] state slice | fb [C][FS] feature
+//   values | uu [C][FS] readouts | xq, xk [C][dk] | ve, hh [C][E] |
+//   jq [parts][C][dk] gradient rows
+struct BwLds {
+  int FS, C, dk, E, parts;
+  __host__ __device__ size_t floats() const {
+    return (size_t)FS * E + 2 * (size_t)C * FS + 2 * (size_t)C * dk + 2 * (size_t)C * E + (size_t)parts * C * dk +
+           3 * (size_t)FS;
+  }
+};
+
+// Pass 2: dL/dq (inter-chunk part), one feature slice of S per workgroup.
+template <typename T>
+__global__ void __launch_bounds__(kBwThreads)
+backward_dq_main(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+                 const float* __restrict__ h, const uint64_t* __restrict__ packed, const float* __restrict__ weight,
+                 int64_t D, float* __restrict__ S_state, float* __restrict__ part, int BH, int n, int dk, int dv,
+                 int C, int FS, int seg0, int seg_len, int first_seg) {
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  const int E = dv + 1;
+  const int parts = kBwThreads / C;
+  uint64_t* tpk = (uint64_t*)lds;
+  float* tw = (float*)(tpk + FS);
+  float* Sl = tw + FS;
+  float* fb = Sl + FS * E;
+  float* uu = fb + C * FS;
+  float* xq = uu + C * FS;
+  float* xk = xq + C * dk;
+  float* ve = xk + C * dk;
+  float* hh = ve + C * E;
+  float* jq = hh + C * E;
+  const int s = blockIdx.x;
+  const int64_t bh = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int64_t f0 = (int64_t)s * FS;
+  const int fs = (int)min<int64_t>(FS, D - f0);
+  float* Sg = S_state + (bh * D + f0) * E;
+  for (int i = tid; i < fs * E; i += kBwThreads) Sl[i] = first_seg ? 0.0f : Sg[i];
+  for (int f = tid; f < fs; f += kBwThreads) {
+    tpk[f] = packed[f0 + f];
+    tw[f] = weight[f0 + f];
+  }
+  const int seg_end = min(n, seg0 + seg_len);
+  for (int t0 = seg0; t0 < seg_end; t0 += C) {
+    const int cn = min(C, n - t0);
+    __syncthreads();
+    bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh);
+    for (int i = tid; i < parts * C * dk; i += kBwThreads) jq[i] = 0.0f;
+    __syncthreads();
+    // u_T[f] = S_{c-1}[f, :] . h_T
+    for (int i = tid; i < cn * fs; i += kBwThreads) {
+      const int t = i / fs;
+      const int f = i - t * fs;
+      float a = 0.0f;
+      for (int j = 0; j < E; ++j) a += Sl[f * E + j] * hh[t * E + j];
+      uu[t * FS + f] = a;
+    }
+    __syncthreads();
+    // dq_T += sum_f u_T[f] d phi_f(q_T) / d q: thread (part, token) takes the
+    // features f = part mod parts into its own gradient row
+    {
+      const int t = tid % C;
+      const int pt = tid / C;
+      if (t < cn) {
+        float* acc = jq + (pt * C + t) * dk;
+        for (int f = pt; f < fs; f += parts) add_feature_gradient(tpk[f], tw[f], uu[t * FS + f], xq + t * dk, acc);
+      }
+    }
+    __syncthreads();
+    float* pout = part + (((int64_t)s * BH + bh) * seg_len + (t0 - seg0)) * dk;
+    for (int i = tid; i < cn * dk; i += kBwThreads) {
+      float a = 0.0f;
+      for (int pt = 0; pt < parts; ++pt) a += jq[pt * C * dk + i];
+      pout[i] = a;
+    }
+    // S_c = S_{c-1} + phi(K_c)^T [V_c | 1]
+    for (int i = tid; i < cn * fs; i += kBwThreads) {
+      const int t = i / fs;
+      const int f = i - t * fs;
+      fb[t * FS + f] = feature_value(tpk[f], tw[f], xk + t * dk);
+    }
+    __syncthreads();
+    for (int i = tid; i < fs * E; i += kBwThreads) {
+      const int f = i / E;
+      const int j = i - f * E;
+      float a = 0.0f;
+      for (int t = 0; t < cn; ++t) a += fb[t * FS + f] * ve[t * E + j];
+      Sl[i] += a;
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < fs * E; i += kBwThreads) Sg[i] = Sl[i];
+}
+
+// Pass 3: dL/dk and dL/dv (inter-chunk parts), chunks in reverse order, one
+// feature slice of U = sum over later tokens of phi(q_T) (x) h_T per workgroup.
+template <typename T>
+__global__ void __launch_bounds__(kBwThreads)
+backward_dkv_main(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+                  const float* __restrict__ h, const uint64_t* __restrict__ packed, const float* __restrict__ weight,
+                  int64_t D, float* __restrict__ U_state, float* __restrict__ part, int BH, int n, int dk, int dv,
+                  int C, int FS, int seg0, int seg_len, int first_seg) {
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  const int E = dv + 1;
+  const int parts = kBwThreads / C;
+  uint64_t* tpk = (uint64_t*)lds;
+  float* tw = (float*)(tpk + FS);
+  float* Ul = tw + FS;
+  float* fb = Ul + FS * E;
+  float* uu = fb + C * FS;
+  float* xq = uu + C * FS;
+  float* xk = xq + C * dk;
+  float* ve = xk + C * dk;
+  float* hh = ve + C * E;
+  float* jq = hh + C * E;
+  const int s = blockIdx.x;
+  const int64_t bh = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int64_t f0 = (int64_t)s * FS;
+  const int fs = (int)min<int64_t>(FS, D - f0);
+  float* Ug = U_state + (bh * D + f0) * E;
+  for (int i = tid; i < fs * E; i += kBwThreads) Ul[i] = first_seg ? 0.0f : Ug[i];
+  for (int f = tid; f < fs; f += kBwThreads) {
+    tpk[f] = packed[f0 + f];
+    tw[f] = weight[f0 + f];
+  }
+  const int seg_end = min(n, seg0 + seg_len);
+  const int PW = dk + dv;  // partial row: dk, then dv
+  for (int t0 = seg0 + (seg_end - 1 - seg0) / C * C; t0 >= seg0; t0 -= C) {
+    const int cn = min(C, n - t0);
+    __syncthreads();
+    bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh);
+    for (int i = tid; i < parts * C * dk; i += kBwThreads) jq[i] = 0.0f;
+    __syncthreads();
+    // phi(k_t) and r_t[f] = U[f, :] . [v_t | 1]
+    for (int i = tid; i < cn * fs; i += kBwThreads) {
+      const int t = i / fs;
+      const int f = i - t * fs;
+      fb[t * FS + f] = feature_value(tpk[f], tw[f], xk + t * dk);
+      float a = 0.0f;
+      for (int j = 0; j < E; ++j) a += Ul[f * E + j] * ve[t * E + j];
+      uu[t * FS + f] = a;
+    }
+    __syncthreads();
+    {
+      const int t = tid % C;
+      const int pt = tid / C;
+      if (t < cn) {
+        float* acc = jq + (pt * C + t) * dk;
+        for (int f = pt; f < fs; f += parts) add_feature_gradient(tpk[f], tw[f], uu[t * FS + f], xk + t * dk, acc);
+      }
+    }
+    __syncthreads();
+    float* pout = part + (((int64_t)s * BH + bh) * seg_len + (t0 - seg0)) * PW;
+    for (int i = tid; i < cn * dk; i += kBwThreads) {
+      const int t = i / dk;
+      const int a = i - t * dk;
+      float sum = 0.0f;
+      for (int pt = 0; pt < parts; ++pt) sum += jq[pt * C * dk + i];
+      pout[t * PW + a] = sum;
+    }
+    // dv_t[j] = sum_f U[f, j] phi_f(k_t)
+    for (int i = tid; i < cn * dv; i += kBwThreads) {
+      const int t = i / dv;
+      const int j = i - t * dv;
+      float a = 0.0f;
+      for (int f = 0; f < fs; ++f) a += Ul[f * E + j] * fb[t * FS + f];
+      pout[t * PW + dk + j] = a;
+    }
+    __syncthreads();
+    // U += phi(Q_c)^T H_c
+    for (int i = tid; i < cn * fs; i += kBwThreads) {
+      const int t = i / fs;
+      const int f = i - t * fs;
+      fb[t * FS + f] = feature_value(tpk[f], tw[f], xq + t * dk);
+    }
+    __syncthreads();
+    for (int i = tid; i < fs * E; i += kBwThreads) {
+      const int f = i / E;
+      const int j = i - f * E;
+      float a = 0.0f;
+      for (int t = 0; t < cn; ++t) a += fb[t * FS + f] * hh[t * E + j];
+      Ul[i] += a;
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < fs * E; i += kBwThreads) Ug[i] = Ul[i];
+}
+
+// Intra-chunk weights of one chunk into LDS: for query row r and key column c
+// (c <= r), W[r][c] = f_P(s_rc) and G[r][c] = (h_r . [v_c|1]) f_{P-1}(s_rc) / sqrt(d_k).
+__device__ void bw_intra_weights(const float* xq, const float* xk, const float* ve, const float* hh, int cn, int C,
+                                 int dk, int E, int P, float* W, float* Gm) {
+  const float scale = 1.0f / sqrtf((float)dk);
+  for (int i = threadIdx.x; i < C * C; i += kBwThreads) {
+    const int r = i / C;
+    const int c = i - r * C;
+    float w = 0.0f, g = 0.0f;
+    if (r < cn && c <= r) {
+      float dot = 0.0f;
+      for (int a = 0; a < dk; ++a) dot += xq[r * dk + a] * xk[c * dk + a];
+      const float sc = dot * scale;
+      float hv = 0.0f;
+      for (int j = 0; j < E; ++j) hv += hh[r * E + j] * ve[c * E + j];
+      w = taylor_horner(sc, P);
+      g = P > 1 ? hv * taylor_horner(sc, P - 1) * scale : 0.0f;
+    }
+    W[i] = w;
+    Gm[i] = g;
+  }
+}
+
+// Pass 1 end: h_T from the forward readout partials plus the intra-chunk term.
+template <typename T>
+__global__ void __launch_bounds__(kBwThreads)
+backward_h_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+                    const T* __restrict__ dy, const float* __restrict__ part, float* __restrict__ h, int BH, int n,
+                    int dk, int dv, int P, int C, int nslices, int seg0, int seg_len) {
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  const int E = dv + 1;
+  float* xq = lds;
+  float* xk = xq + C * dk;
+  float* ve = xk + C * dk;
+  float* O = ve + C * E;   // [C][E]
+  float* W = O + C * E;    // [C][C]
+  const int64_t bh = blockIdx.y;
+  const int t0 = seg0 + blockIdx.x * C;
+  if (t0 >= n) return;
+  const int cn = min(C, n - t0);
+  const int tid = threadIdx.x;
+  const float scale = 1.0f / sqrtf((float)dk);
+  const int64_t off = (bh * n + t0) * (int64_t)dk;
+  for (int i = tid; i < C * dk; i += kBwThreads) {
+    const int t = i / dk;
+    xq[i] = t < cn ? to_f32(q[off + i]) : 0.0f;
+    xk[i] = t < cn ? to_f32(k[off + i]) : 0.0f;
+  }
+  for (int i = tid; i < C * E; i += kBwThreads) {
+    const int t = i / E;
+    const int j = i - t * E;
+    ve[i] = t < cn ? ((j < dv) ? to_f32(v[(bh * n + t0 + t) * (int64_t)dv + j]) : 1.0f) : 0.0f;
+  }
+  __syncthreads();
+  for (int i = tid; i < C * C; i += kBwThreads) {
+    const int r = i / C;
+    const int c = i - r * C;
+    float w = 0.0f;
+    if (r < cn && c <= r) {
+      float dot = 0.0f;
+      for (int a = 0; a < dk; ++a) dot += xq[r * dk + a] * xk[c * dk + a];
+      w = taylor_horner(dot * scale, P);
+    }
+    W[i] = w;
+  }
+  __syncthreads();
+  for (int o = tid; o < cn * E; o += kBwThreads) {
+    const int r = o / E;
+    const int j = o - r * E;
+    float acc = 0.0f;
+    for (int c = 0; c <= r; ++c) acc += W[r * C + c] * ve[c * E + j];
+    for (int s = 0; s < nslices; ++s) acc += part[(((int64_t)s * BH + bh) * seg_len + (t0 - seg0) + r) * E + j];
+    O[o] = acc;
+  }
+  __syncthreads();
+  for (int r = tid; r < cn; r += kBwThreads) {
+    const float Z = O[r * E + dv];
+    const T* g = dy + (bh * n + t0 + r) * (int64_t)dv;
+    float gy = 0.0f;
+    for (int j = 0; j < dv; ++j) gy += to_f32(g[j]) * (O[r * E + j] / Z);
+    float* hr = h + (bh * n + t0 + r) * (int64_t)E;
+    for (int j = 0; j < dv; ++j) hr[j] = to_f32(g[j]) / Z;
+    hr[dv] = -gy / Z;
+  }
+}
+
+// Pass 2 end: dq = sum of the slices' partials + intra-chunk part.
+template <typename T>
+__global__ void __launch_bounds__(kBwThreads)
+backward_dq_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+                     const float* __restrict__ h, const float* __restrict__ part, T* __restrict__ dq, int BH, int n,
+                     int dk, int dv, int P, int C, int nslices, int seg0, int seg_len) {
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  const int E = dv + 1;
+  float* xq = lds;
+  float* xk = xq + C * dk;
+  float* ve = xk + C * dk;
+  float* hh = ve + C * E;
+  float* W = hh + C * E;
+  float* Gm = W + C * C;
+  const int64_t bh = blockIdx.y;
+  const int t0 = seg0 + blockIdx.x * C;
+  if (t0 >= n) return;
+  const int cn = min(C, n - t0);
+  bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh);
+  __syncthreads();
+  bw_intra_weights(xq, xk, ve, hh, cn, C, dk, E, P, W, Gm);
+  __syncthreads();
+  for (int i = threadIdx.x; i < cn * dk; i += kBwThreads) {
+    const int r = i / dk;
+    const int a = i - r * dk;
+    float acc = 0.0f;
+    for (int c = 0; c <= r; ++c) acc += Gm[r * C + c] * xk[c * dk + a];
+    for (int s = 0; s < nslices; ++s) acc += part[(((int64_t)s * BH + bh) * seg_len + (t0 - seg0) + r) * dk + a];
+    dq[(bh * n + t0 + r) * (int64_t)dk + a] = from_f32<T>(acc);
+  }
+}
+
+// Pass 3 end: dk, dv = sum of the slices' partials + intra-chunk parts.
+template <typename T>
+__global__ void __launch_bounds__(kBwThreads)
+backward_dkv_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+                      const float* __restrict__ h, const float* __restrict__ part, T* __restrict__ dk_out,
+                      T* __restrict__ dv_out, int BH, int n, int dk, int dv, int P, int C, int nslices, int seg0,
+                      int seg_len) {
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  const int E = dv + 1;
+  const int PW = dk + dv;
+  float* xq = lds;
+  float* xk = xq + C * dk;
+  float* ve = xk + C * dk;
+  float* hh = ve + C * E;
+  float* W = hh + C * E;
+  float* Gm = W + C * C;
+  const int64_t bh = blockIdx.y;
+  const int t0 = seg0 + blockIdx.x * C;
+  if (t0 >= n) return;
+  const int cn = min(C, n - t0);
+  bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh);
+  __syncthreads();
+  bw_intra_weights(xq, xk, ve, hh, cn, C, dk, E, P, W, Gm);
+  __syncthreads();
+  for (int i = threadIdx.x; i < cn * PW; i += kBwThreads) {
+    const int c = i / PW;
+    const int a = i - c * PW;
+    float acc = 0.0f;
+    if (a < dk) {
+      for (int r = c; r < cn; ++r) acc += Gm[r * C + c] * xq[r * dk + a];
+    } else {
+      for (int r = c; r < cn; ++r) acc += W[r * C + c] * hh[r * E + (a - dk)];
+    }
+    for (int s = 0; s < nslices; ++s) acc += part[(((int64_t)s * BH + bh) * seg_len + (t0 - seg0) + c) * PW + a];
+    if (a < dk)
+      dk_out[(bh * n + t0 + c) * (int64_t)dk + a] = from_f32<T>(acc);
+    else
+      dv_out[(bh * n + t0 + c) * (int64_t)dv + (a - dk)] = from_f32<T>(acc);
+  }
+}
+
+}  // namespace
+
+bool plan_backward(int64_t D, int BH, int n, int dk, int dv, int chunk, size_t max_ws_bytes, BackwardPlan* plan,
+                   PrefillGenericPlan* fwd) {
+  if (dk > kMaxBackwardDim || dv > kMaxBackwardDim) return false;
+  if (chunk != 16 && chunk != 32 && chunk != 64) return false;
+  if (!plan_prefill_generic(D, BH, n, dk, dv, chunk, max_ws_bytes, fwd)) return false;
+  const int E = dv + 1;
+  const int C = chunk;
+  BwLds L{0, C, dk, E, kBwThreads / C};
+  const size_t budget = 150 * 1024;
+  const size_t fixed = sizeof(float) * L.floats();
+  const size_t per_feature = sizeof(float) * ((size_t)E + 2 * (size_t)C + 3);
+  if (fixed + 8 * per_feature > budget) return false;
+  int64_t fs = (int64_t)((budget - fixed) / per_feature);
+  fs = std::min<int64_t>(fs, 512);
+  const int64_t want = (512 + BH - 1) / BH;  // about two workgroups per CU
+  fs = std::min<int64_t>(fs, std::max<int64_t>(16, (D + want - 1) / want));
+  fs = std::max<int64_t>(1, std::min<int64_t>(fs, D));
+  L.FS = (int)fs;
+  plan->fs = (int)fs;
+  plan->nslices = (int)((D + fs - 1) / fs);
+  plan->lds_main = sizeof(float) * L.floats();
+  plan->lds_h = sizeof(float) * (2 * (size_t)C * dk + 2 * (size_t)C * E + (size_t)C * C);
+  plan->lds_fin = sizeof(float) * (2 * (size_t)C * dk + 2 * (size_t)C * E + 2 * (size_t)C * C);
+  // partial rows per token: the forward readout (E per forward slice), dq (dk),
+  // dk and dv (dk + dv) per backward slice
+  const size_t per_token = sizeof(float) * (size_t)BH *
+                           std::max<size_t>((size_t)fwd->nslices * E, (size_t)plan->nslices * (dk + dv));
+  int64_t seg = (int64_t)(max_ws_bytes / per_token) / C * C;
+  if (seg < C) seg = C;
+  const int64_t n_round = ((int64_t)std::max(n, 1) + C - 1) / C * C;
+  plan->seg_len = (int)std::min<int64_t>(seg, n_round);
+  plan->partial_bytes = per_token * (size_t)plan->seg_len;
+  fwd->seg_len = plan->seg_len;
+  plan->h_bytes = sizeof(float) * (size_t)BH * n * E;
+  plan->state_bytes = sizeof(float) * (size_t)BH * D * E;
+  return true;
+}
+
+template <typename T>
+static hipError_t launch_backward_typed(const T* q, const T* k, const T* v, const T* dy, T* dq, T* dk, T* dv_out,
+                                        int BH, int n, int dk_, int dv, int P, int chunk, const DevTable& t,
+                                        const BackwardPlan& plan, const PrefillGenericPlan& fwd, float* h,
+                                        float* state, float* partial, hipStream_t s) {
+  const int C = chunk;
+  hipError_t e;
+  if ((e = hipFuncSetAttribute((const void*)backward_dq_main<T>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)plan.lds_main)) != hipSuccess)
+    return e;
+  if ((e = hipFuncSetAttribute((const void*)backward_dkv_main<T>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)plan.lds_main)) != hipSuccess)
+    return e;
+  if ((e = hipFuncSetAttribute((const void*)backward_h_finalize<T>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)plan.lds_h)) != hipSuccess)
+    return e;
+  if ((e = hipFuncSetAttribute((const void*)backward_dq_finalize<T>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)plan.lds_fin)) != hipSuccess)
+    return e;
+  if ((e = hipFuncSetAttribute((const void*)backward_dkv_finalize<T>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)plan.lds_fin)) != hipSuccess)
+    return e;
+  const int nseg = (n + plan.seg_len - 1) / plan.seg_len;
+  // pass 1: the forward readout of each segment, then h
+  for (int sg = 0; sg < nseg; ++sg) {
+    const int seg0 = sg * plan.seg_len;
+    if ((e = launch_prefill_generic_readout(q, k, v, std::is_same<T, bf16_t>::value, BH, n, dk_, dv, C, t, fwd,
+                                            state, partial, seg0, plan.seg_len, sg == 0, s)) != hipSuccess)
+      return e;
+    const int nchunks = (std::min(plan.seg_len, n - seg0) + C - 1) / C;
+    hipLaunchKernelGGL(backward_h_finalize<T>, dim3((unsigned)nchunks, (unsigned)BH), dim3(kBwThreads),
+                       plan.lds_h, s, q, k, v, dy, partial, h, BH, n, dk_, dv, P, C, fwd.nslices, seg0,
+                       plan.seg_len);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  // pass 2: dq
+  for (int sg = 0; sg < nseg; ++sg) {
+    const int seg0 = sg * plan.seg_len;
+    hipLaunchKernelGGL(backward_dq_main<T>, dim3((unsigned)plan.nslices, (unsigned)BH), dim3(kBwThreads),
+                       plan.lds_main, s, q, k, v, h, t.packed, t.weight, t.D, state, partial, BH, n, dk_, dv, C,
+                       plan.fs, seg0, plan.seg_len, sg == 0 ? 1 : 0);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const int nchunks = (std::min(plan.seg_len, n - seg0) + C - 1) / C;
+    hipLaunchKernelGGL(backward_dq_finalize<T>, dim3((unsigned)nchunks, (unsigned)BH), dim3(kBwThreads),
+                       plan.lds_fin, s, q, k, v, h, partial, dq, BH, n, dk_, dv, P, C, plan.nslices, seg0,
+                       plan.seg_len);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  // pass 3: dk, dv, segments from the last
+  for (int sg = nseg - 1; sg >= 0; --sg) {
+    const int seg0 = sg * plan.seg_len;
+    hipLaunchKernelGGL(backward_dkv_main<T>, dim3((unsigned)plan.nslices, (unsigned)BH), dim3(kBwThreads),
+                       plan.lds_main, s, q, k, v, h, t.packed, t.weight, t.D, state, partial, BH, n, dk_, dv, C,
+                       plan.fs, seg0, plan.seg_len, sg == nseg - 1 ? 1 : 0);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const int nchunks = (std::min(plan.seg_len, n - seg0) + C - 1) / C;
+    hipLaunchKernelGGL(backward_dkv_finalize<T>, dim3((unsigned)nchunks, (unsigned)BH), dim3(kBwThreads),
+                       plan.lds_fin, s, q, k, v, h, partial, dk, dv_out, BH, n, dk_, dv, P, C, plan.nslices, seg0,
+                       plan.seg_len);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_backward(const void* q, const void* k, const void* v, const void* dy, void* dq, void* dk,
+                           void* dv, bool bf16, int BH, int n, int dk_, int dv_, int P, int chunk, const DevTable& t,
+                           const BackwardPlan& plan, const PrefillGenericPlan& fwd, float* h, float* state,
+                           float* partial, hipStream_t s) {
+  if (bf16)
+    return launch_backward_typed<bf16_t>((const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, (const bf16_t*)dy,
+                                         (bf16_t*)dq, (bf16_t*)dk, (bf16_t*)dv, BH, n, dk_, dv_, P, chunk, t, plan,
+                                         fwd, h, state, partial, s);
+  return launch_backward_typed<float>((const float*)q, (const float*)k, (const float*)v, (const float*)dy,
+                                      (float*)dq, (float*)dk, (float*)dv, BH, n, dk_, dv_, P, chunk, t, plan, fwd, h,
+                                      state, partial, s);
+}
+
+}  // namespace sata

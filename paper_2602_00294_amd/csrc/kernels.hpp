@@ -81,6 +81,34 @@ hipError_t launch_prefill_generic(const void* q, const void* k, const void* v, v
                                   const PrefillGenericPlan& plan, float* S_state, float* partial,
                                   hipStream_t s, int qg = 1);
 
+// One segment of the float32 prefill's main kernel only: the partial readouts
+// of tokens [seg0, seg0 + plan.seg_len) against S_state, which it carries from
+// the previous segment (first: from zero).
+hipError_t launch_prefill_generic_readout(const void* q, const void* k, const void* v, bool bf16, int BH, int n,
+                                          int dk, int dv, int chunk, const DevTable& t,
+                                          const PrefillGenericPlan& plan, float* S_state, float* partial, int seg0,
+                                          int seg_len, bool first, hipStream_t s);
+
+// ---- backward ----------------------------------------------------------------
+constexpr int kMaxBackwardDim = 64;
+struct BackwardPlan {
+  int fs = 0;              // features per slice of the scan kernels
+  int nslices = 0;         // slices per head
+  int seg_len = 0;         // tokens per segment (multiple of the chunk)
+  size_t lds_main = 0, lds_h = 0, lds_fin = 0;
+  size_t partial_bytes = 0;  // partial sums of one segment
+  size_t h_bytes = 0;        // dL/do for every token, float32 [BH][n][d_v+1]
+  size_t state_bytes = 0;    // one float32 state [BH][D][d_v+1]
+};
+// False if d_k or d_v exceeds kMaxBackwardDim, the chunk is not 16, 32 or 64,
+// or no slice fits on chip.  Also fills the forward plan of the first pass.
+bool plan_backward(int64_t D, int BH, int n, int dk, int dv, int chunk, size_t max_ws_bytes, BackwardPlan* plan,
+                   PrefillGenericPlan* fwd);
+hipError_t launch_backward(const void* q, const void* k, const void* v, const void* dy, void* dq, void* dk,
+                           void* dv, bool bf16, int BH, int n, int dk_, int dv_, int P, int chunk, const DevTable& t,
+                           const BackwardPlan& plan, const PrefillGenericPlan& fwd, float* h, float* state,
+                           float* partial, hipStream_t s);
+
 // ---- helpers -----------------------------------------------------------------
 hipError_t launch_fill_zero(float* p, int64_t count, hipStream_t s);
 

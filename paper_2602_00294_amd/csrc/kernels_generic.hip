@@ -995,4 +995,29 @@ hipError_t launch_prefill_generic(const void* q, const void* k, const void* v, v
   return hipSuccess;
 }
 
+hipError_t launch_prefill_generic_readout(const void* q, const void* k, const void* v, bool bf16, int BH, int n,
+                                          int dk, int dv, int chunk, const DevTable& t,
+                                          const PrefillGenericPlan& plan, float* S_state, float* partial, int seg0,
+                                          int seg_len, bool first, hipStream_t s) {
+  const int C = chunk;
+  hipError_t e;
+  dim3 g1((unsigned)plan.nslices, (unsigned)BH);
+  if (bf16) {
+    if ((e = hipFuncSetAttribute((const void*)prefill_generic_main<bf16_t>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)plan.lds_main)) != hipSuccess)
+      return e;
+    hipLaunchKernelGGL(prefill_generic_main<bf16_t>, g1, dim3(kThreads), plan.lds_main, s, (const bf16_t*)q,
+                       (const bf16_t*)k, (const bf16_t*)v, t.packed, t.weight, t.D, S_state, partial, BH, n, dk, dv,
+                       C, plan.fs, seg0, seg_len, first ? 1 : 0, 1);
+  } else {
+    if ((e = hipFuncSetAttribute((const void*)prefill_generic_main<float>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)plan.lds_main)) != hipSuccess)
+      return e;
+    hipLaunchKernelGGL(prefill_generic_main<float>, g1, dim3(kThreads), plan.lds_main, s, (const float*)q,
+                       (const float*)k, (const float*)v, t.packed, t.weight, t.D, S_state, partial, BH, n, dk, dv, C,
+                       plan.fs, seg0, seg_len, first ? 1 : 0, 1);
+  }
+  return hipGetLastError();
+}
+
 }  // namespace sata

@@ -449,6 +449,40 @@ sata_status sata_prefill_grouped(const void* q, const void* k, const void* v, sa
   return ok();
 }
 
+sata_status sata_backward(const void* q, const void* k, const void* v, const void* dy, sata_dtype dt, int B, int H,
+                          int n, int d_k, int d_v, int P, int chunk, void* dq, void* dk, void* dv, void* stream) {
+  if (!valid_dtype(dt)) return fail(SATA_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
+  if (B < 1 || H < 1) return fail(SATA_ERR_INVALID_ARG, "B=%d H=%d must be >= 1", B, H);
+  if (n < 0) return fail(SATA_ERR_INVALID_ARG, "n=%d < 0", n);
+  int64_t D = 0;
+  sata_status st = check_dims(d_k, d_v, P, &D);
+  if (st != SATA_OK) return st;
+  if ((int64_t)B * H > kMaxHeads) return fail(SATA_ERR_TOO_LARGE, "B*H=%lld exceeds %d", (long long)B * H, kMaxHeads);
+  if (chunk != 16 && chunk != 32 && chunk != 64)
+    return fail(SATA_ERR_UNSUPPORTED, "chunk=%d; the backward supports 16, 32, 64", chunk);
+  if (d_k > sata::kMaxBackwardDim || d_v > sata::kMaxBackwardDim)
+    return fail(SATA_ERR_UNSUPPORTED, "the backward supports d_k, d_v <= %d", sata::kMaxBackwardDim);
+  if (n == 0) return ok();
+  if (!q || !k || !v || !dy || !dq || !dk || !dv) return fail(SATA_ERR_INVALID_ARG, "null tensor pointer");
+  const int BH = B * H;
+  sata::BackwardPlan plan;
+  sata::PrefillGenericPlan fwd;
+  if (!sata::plan_backward(D, BH, n, d_k, d_v, chunk, kMaxWorkspace, &plan, &fwd))
+    return fail(SATA_ERR_UNSUPPORTED, "no backward slice fits on chip for d_k=%d d_v=%d chunk=%d", d_k, d_v, chunk);
+  hipStream_t s = (hipStream_t)stream;
+  sata::DevTable t;
+  if ((st = get_table(d_k, P, s, &t)) != SATA_OK) return st;
+  void* ws = nullptr;
+  if ((st = get_workspace(plan.h_bytes + plan.state_bytes + plan.partial_bytes, s, &ws)) != SATA_OK) return st;
+  float* h = (float*)ws;
+  float* state = (float*)((char*)ws + plan.h_bytes);
+  float* partial = (float*)((char*)ws + plan.h_bytes + plan.state_bytes);
+  hipError_t e = sata::launch_backward(q, k, v, dy, dq, dk, dv, dt == SATA_BF16, BH, n, d_k, d_v, P, chunk, t, plan,
+                                       fwd, h, state, partial, s);
+  if (e != hipSuccess) return hip_fail(e, "backward launch");
+  return ok();
+}
+
 sata_status sata_decode_step(float* S, const void* q, const void* k, const void* v, sata_dtype dt, int B,
                              int H, int d_k, int d_v, int P, void* y, void* stream) {
   return decode_step(S, nullptr, q, k, v, dt, B, H, d_k, d_v, P, y, stream);

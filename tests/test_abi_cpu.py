@@ -117,6 +117,16 @@ def test_prefill_grouped_validation(lib):
     assert g(FAKE, FAKE, FAKE, 5, 1, 1, 2, 8, 4, 4, 4, 64, FAKE, NULL, NULL) == -1      # dtype
 
 
+def test_backward_validation(lib):
+    # (q, k, v, dy, dtype, B, H, n, d_k, d_v, P, chunk, dq, dk, dv, stream)
+    b = lib.sata_backward
+    assert b(FAKE, FAKE, FAKE, FAKE, 0, 1, 1, 8, 4, 4, 4, 128, FAKE, FAKE, FAKE, NULL) == -2   # chunk 128
+    assert b(FAKE, FAKE, FAKE, FAKE, 0, 1, 1, 8, 65, 4, 2, 64, FAKE, FAKE, FAKE, NULL) == -2   # d_k = 65
+    assert b(FAKE, FAKE, FAKE, FAKE, 0, 1, 1, 8, 4, 4, 9, 64, FAKE, FAKE, FAKE, NULL) == -1    # P = 9
+    assert b(FAKE, FAKE, FAKE, NULL, 0, 1, 1, 8, 4, 4, 4, 64, FAKE, FAKE, FAKE, NULL) == -1    # null dy
+    assert b(FAKE, FAKE, FAKE, FAKE, 0, 1, 1, 0, 4, 4, 4, 64, FAKE, FAKE, FAKE, NULL) == 0     # n = 0
+
+
 def test_status_strings(lib):
     for code in (0, -1, -2, -3, -4):
         assert lib.sata_status_string(code)
