@@ -40,6 +40,8 @@ its own line in the same form:
               steps (per-step time), and the CPU leg checks decoded rows at the
               longest context, far beyond 2^24 tokens, against the oracle
               (Sec. 3.2: cost per token that does not grow with the context);
+  backward    B=8, H=32, n=2048, d_k=d_v=32, P=4, bf16: dL/dq, dL/dk, dL/dv
+              (float32 arithmetic), checked on two heads against the oracle;
   decode_grouped B=8, 32 query heads, d_k=d_v=32, P=4, bf16: an 8192-token
               prefill of the key/value heads, then 1024 grouped decode steps
               for G = 2, 4, 8 query heads per key/value head (16, 8, 4
@@ -123,7 +125,7 @@ def parse():
     ap.add_argument("--cpu-sample-decode-rows", type=int, default=128)
     ap.add_argument("--workload", default="headline", choices=["headline", "decode_d16", "large_d64", "sweep_d16",
                                                                   "decode_hbm", "error_study", "context_sweep",
-                                                                  "decode_grouped"])
+                                                                  "decode_grouped", "backward"])
     ap.add_argument("--seq-len", type=int, default=0,
                     help="error_study only: tokens per sequence (default 100000)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -549,6 +551,77 @@ CONTEXT_SWEEP = [(8, 8), (16, 8), (32, 8), (64, 7)]  # (d, largest power of ten 
 CONTEXT_DECODE = 64
 
 
+def backward_flops_per_head_token(dk, dv, P, C):
+    """Algorithmic work of the backward per head-token: the forward readout
+    recomputed (2 D (d_v+1)), the forward scan's S h readout and state update
+    (2 x 2 D (d_v+1)), the reverse scan's U [v|1] readout, U^T phi(k) and U
+    update (2 D (d_v+1) + 2 D d_v + 2 D (d_v+1)), the two Jacobian products of
+    the feature map (2 x 2 (P-1) D), and the intra-chunk terms (about
+    (C+1)(3 d_k + 2 d_v + 3) per token)."""
+    D = feature_count(dk, P)
+    E = dv + 1
+    return 2 * D * E + 4 * D * E + (4 * D * E + 2 * D * dv) + 4 * (P - 1) * D + (C + 1) * (3 * dk + 2 * dv + 3)
+
+
+def run_backward(args, sata, torch):
+    """sata_backward on B=8, H=32, n=2048, d_k=d_v=32, P=4, bf16 (the
+    benchmark's head shape, a quarter of its length); the CPU leg checks two
+    heads' gradients against the float64 oracle."""
+    import numpy as np
+
+    import sata_synth as syn
+    Bw, Hw, n, d, Pw, C, wid = 8, 32, 2048, 32, 4, 64, 7
+    arrs = [np.empty((Bw, Hw, n, d), np.float32) for _ in range(4)]
+    for b in range(Bw):
+        for h in range(Hw):
+            arrs[0][b, h], arrs[1][b, h], arrs[2][b, h] = syn.make_head(wid, b, h, n, d, d, "bf16")
+            arrs[3][b, h] = syn.head_stream(wid, b, h, 3, (n, d), "bf16")
+    dev = [torch.from_numpy(a).to("cuda").to(torch.bfloat16) for a in arrs]
+    for _ in range(args.warmup):
+        sata.backward(*dev, Pw, C)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    for _ in range(args.steps):
+        out = sata.backward(*dev, Pw, C)
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / args.steps
+    flops = backward_flops_per_head_token(d, d, Pw, C) * Bw * Hw * n
+    ach = flops / (ms * 1e-3) / 1e12
+    line = {
+        "metric": "backward tokens/s (d_k=32,P=4); % float32 roofline",
+        "value": Bw * n / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"backward: dL/dq, dL/dk, dL/dv of the causal prefill, B={Bw} H={Hw} n={n} "
+                               f"d_k=d_v={d} P={Pw} bf16 chunk={C}, float32 arithmetic",
+                   "global_batch": Bw, "seq_len": n, "heads": Hw, "d_k": d, "d_v": d, "P": Pw, "chunk": C,
+                   "parallelism": "single GPU"},
+        "roofline": {"kernel": "sata_backward (all launches of one call)", "bound": "alu", "achieved": ach,
+                     "peak": PEAK_F32_TFLOPS, "unit": "TFLOP/s", "frac": ach / PEAK_F32_TFLOPS, "traffic": None,
+                     "work_per_launch": flops},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+        got = [o.float().cpu().numpy() for o in out]
+        errs = {}
+        t = 0.0
+        for (b, h) in ((0, 0), (Bw - 1, Hw - 1)):
+            t0 = time.perf_counter()
+            want = oracle.taylor_attention_backward(arrs[0][b, h], arrs[1][b, h], arrs[2][b, h], arrs[3][b, h], Pw)
+            t += time.perf_counter() - t0
+            for name, g_, w_ in zip(("dq", "dk", "dv"), got, want):
+                errs[f"b{b}h{h}_{name}"] = float(np.linalg.norm(g_[b, h] - w_) / np.linalg.norm(w_))
+        line["cpu_baseline"] = {"value": 2 * n / t / Hw, "unit": "tokens/s", "cores": threads,
+                                "blas_threads": blas_threads(), "kind": "oracle",
+                                "sample": f"2 of {Bw * Hw} heads, full {n}-token backward by the direct float64 "
+                                          "definition; rate scaled to whole-batch tokens",
+                                "seconds": t, "parity_rel_err": errs}
+    return line
+
+
 def run_context_sweep(args, sata, torch):
     """Prefill of contexts 10^3 ... 10^8 tokens, then decode steps, per head
     size; time and device memory per token.  Inputs: sata_synth.long_head."""
@@ -662,6 +735,9 @@ def main():
     assert torch.cuda.is_available(), "no GPU"
     if args.workload == "decode_grouped":
         print(json.dumps(run_decode_grouped(args, sata, torch)), flush=True)
+        return
+    if args.workload == "backward":
+        print(json.dumps(run_backward(args, sata, torch)), flush=True)
         return
     if args.workload == "context_sweep":
         print(json.dumps(run_context_sweep(args, sata, torch)), flush=True)
