@@ -280,7 +280,7 @@ def run_workload(args, sata, torch):
         dec_ms = sum(e[1].elapsed_time(e[2]) for e in events) / args.steps if n_dec else 0.0
         t_total += pre_ms + dec_ms
         flops = prefill_flops_per_head_token(d, d, Pw, CHUNK) * Bw * Hw * n
-        mfma = dt == "bf16" and Pw == 4 and d in (16, 32)  # the matrix-core prefill shapes
+        mfma = sata.prefill_operands(tdt, Bw, Hw, n, d, d, Pw, CHUNK) == "bf16"  # on the matrix cores
         peak = PEAK_BF16_TFLOPS if mfma else PEAK_F32_TFLOPS
         ach = flops / (pre_ms * 1e-3) / 1e12
         roof_pre = {"kernel": "sata_prefill (all launches of one call)", "bound": "mfma" if mfma else "alu",

@@ -6,10 +6,18 @@
 
 namespace sata {
 
+// Zero entries (degree 0, weight 0) that follow the D features of a device
+// table, so that kernels may read whole slices of up to this many features
+// past the last one without a bounds check.
+constexpr int kTablePad = 4096;
+// Features per block of the generation program (table.hpp build_gen_program).
+constexpr int kGenBlock = 32;
+
 // One (d, P) feature table resident on a device (see table.hpp for its layout).
 struct DevTable {
-  const uint64_t* packed = nullptr;  // [D] packed multi-indices
-  const float* weight = nullptr;     // [D] feature weights
+  const uint64_t* packed = nullptr;  // [D + kTablePad] packed multi-indices
+  const float* weight = nullptr;     // [D + kTablePad] feature weights
+  const uint32_t* gen = nullptr;     // [D + kTablePad][2] generation program (blocks of kGenBlock)
   int64_t D = 0;
   int d = 0;
   int P = 0;
@@ -88,6 +96,12 @@ hipError_t launch_prefill_generic_readout(const void* q, const void* k, const vo
                                           int dk, int dv, int chunk, const DevTable& t,
                                           const PrefillGenericPlan& plan, float* S_state, float* partial, int seg0,
                                           int seg_len, bool first, hipStream_t s);
+
+// One segment of the float32 prefill's finalize: adds nslices partial readouts
+// ([slice][BH][seg_len][d_v+1]), the intra-chunk term, and divides.
+hipError_t launch_prefill_generic_finalize(const void* q, const void* k, const void* v, void* y, bool bf16, int BH,
+                                           int n, int dk, int dv, int P, int chunk, int nslices, int seg0,
+                                           int seg_len, const float* partial, hipStream_t s, int qg);
 
 // ---- backward ----------------------------------------------------------------
 constexpr int kMaxBackwardDim = 64;

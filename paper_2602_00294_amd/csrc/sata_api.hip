@@ -13,6 +13,7 @@
 
 #include "kernels.hpp"
 #include "prefill_blocks.hpp"
+#include "prefill_feat.hpp"
 #include "prefill_mfma.hpp"
 #include "sata.h"
 #include "table.hpp"
@@ -44,6 +45,8 @@ struct TableEntry {
   sata::FeatureTable host;
   uint64_t* packed = nullptr;
   float* weight = nullptr;
+  uint32_t* gen = nullptr;
+  std::vector<uint32_t> host_gen;
 };
 
 struct Workspace {
@@ -97,26 +100,38 @@ sata_status get_table(int d, int P, hipStream_t stream, sata::DevTable* out) {
   if (it == dc.tables.end()) {
     TableEntry ent;
     ent.host = sata::build_table(d, P);
-    const size_t D = (size_t)ent.host.D;
-    if ((e = hipMalloc(&ent.packed, D * sizeof(uint64_t))) != hipSuccess) return hip_fail(e, "hipMalloc(table)");
-    if ((e = hipMalloc(&ent.weight, D * sizeof(float))) != hipSuccess) {
+    ent.host_gen = sata::build_gen_program(ent.host, sata::kTablePad, sata::kGenBlock);
+    // the device copy ends in kTablePad zero entries
+    ent.host.packed.resize(ent.host.packed.size() + sata::kTablePad, 0);
+    ent.host.weight.resize(ent.host.weight.size() + sata::kTablePad, 0.0f);
+    const size_t D = (size_t)ent.host.D + sata::kTablePad;
+    auto release = [&ent]() {
       hipFree(ent.packed);
+      hipFree(ent.weight);
+      hipFree(ent.gen);
+    };
+    if ((e = hipMalloc(&ent.packed, D * sizeof(uint64_t))) != hipSuccess ||
+        (e = hipMalloc(&ent.weight, D * sizeof(float))) != hipSuccess ||
+        (e = hipMalloc(&ent.gen, 2 * D * sizeof(uint32_t))) != hipSuccess) {
+      release();
       return hip_fail(e, "hipMalloc(table)");
     }
-    // The host copy lives in the cache, so an asynchronous copy is safe.
+    // The host copies live in the cache, so asynchronous copies are safe.
     e = hipMemcpyAsync(ent.packed, ent.host.packed.data(), D * sizeof(uint64_t), hipMemcpyHostToDevice, stream);
     if (e == hipSuccess)
       e = hipMemcpyAsync(ent.weight, ent.host.weight.data(), D * sizeof(float), hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(ent.gen, ent.host_gen.data(), 2 * D * sizeof(uint32_t), hipMemcpyHostToDevice, stream);
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
     if (e != hipSuccess) {
-      hipFree(ent.packed);
-      hipFree(ent.weight);
+      release();
       return hip_fail(e, "uploading feature table");
     }
     it = dc.tables.emplace(key, std::move(ent)).first;
   }
   out->packed = it->second.packed;
   out->weight = it->second.weight;
+  out->gen = it->second.gen;
   out->D = it->second.host.D;
   out->d = d;
   out->P = P;
@@ -135,6 +150,7 @@ sata_status find_table(int d, int P, sata::DevTable* out) {
     if (it != dc->second.tables.end()) {
       out->packed = it->second.packed;
       out->weight = it->second.weight;
+      out->gen = it->second.gen;
       out->D = it->second.host.D;
       out->d = d;
       out->P = P;
@@ -249,13 +265,17 @@ sata_status check_prefill_args(sata_dtype dt, int B, int H, int n, int d_k, int 
   return SATA_OK;
 }
 
-enum class PrefillPath { kMfma32, kBlocks, kFloat32 };
+enum class PrefillPath { kMfma32, kBlocks, kFeat, kFloat32 };
 
 // The kernel family that serves a validated prefill request.
 PrefillPath prefill_path(sata_dtype dt, int BH, int n, int d_k, int d_v, int P, int chunk) {
   sata::MfmaPrefillPlan mp;
   if (dt == SATA_BF16 && sata::plan_prefill_mfma(BH, n, d_k, d_v, P, chunk, &mp)) return PrefillPath::kMfma32;
   if (dt == SATA_BF16 && sata::plan_prefill_blocks(BH, n, d_k, d_v, P, chunk, &mp)) return PrefillPath::kBlocks;
+  sata::FeatPrefillPlan fp;
+  if (dt == SATA_BF16 && sata::plan_prefill_feat(sata::feature_count(d_k, P), BH, n, d_k, d_v, P, chunk,
+                                                 kMaxWorkspace, &fp))
+    return PrefillPath::kFeat;
   return PrefillPath::kFloat32;
 }
 
@@ -291,6 +311,18 @@ sata_status prefill_dispatch(const void* q, const void* k, const void* v, sata_d
     if ((st = get_workspace(mp.workspace_bytes, s, &ws)) != SATA_OK) return st;
     e = sata::launch_prefill_blocks(q, k, v, y, S_out, BH, n, d_k, d_v, P, chunk, mp, ws, s, qg);
     if (e != hipSuccess) return hip_fail(e, "prefill (matrix-core, per-block) launch");
+    return ok();
+  }
+
+  sata::FeatPrefillPlan fp;
+  if (path == PrefillPath::kFeat && sata::plan_prefill_feat(D, BH, n, d_k, d_v, P, chunk, kMaxWorkspace, &fp)) {
+    const size_t state_bytes = S_out ? 0 : sizeof(float) * (size_t)BH * D * E;
+    void* ws = nullptr;
+    if ((st = get_workspace(fp.partial_bytes + state_bytes, s, &ws)) != SATA_OK) return st;
+    float* partial = (float*)ws;
+    float* S_state = S_out ? S_out : (float*)((char*)ws + fp.partial_bytes);
+    e = sata::launch_prefill_feat(q, k, v, y, BH, n, d_k, d_v, P, t, fp, S_state, partial, s, qg);
+    if (e != hipSuccess) return hip_fail(e, "prefill (matrix-core, generated features) launch");
     return ok();
   }
 
@@ -589,6 +621,7 @@ void sata_release(void) {
     for (auto& t : kv.second.tables) {
       hipFree(t.second.packed);
       hipFree(t.second.weight);
+      hipFree(t.second.gen);
     }
     for (auto& w : kv.second.workspaces) hipFree(w.second.ptr);
     for (auto& w : kv.second.counters) hipFree(w.second.ptr);

@@ -96,6 +96,7 @@ def test_grouped_decode_deterministic_and_g1_is_decode_step(sata):
 @pytest.mark.parametrize("B,Hkv,G,n,d,P,chunk,dtype", [
     (1, 2, 4, 150, 32, 4, 64, "bf16"),   # the d = 32 matrix-core kernel
     (2, 2, 2, 97, 16, 4, 32, "bf16"),    # the per-block matrix-core kernel
+    (1, 3, 2, 100, 8, 3, 64, "bf16"),    # the generated-feature matrix-core kernel
     (1, 3, 2, 70, 8, 4, 64, "f32"),      # the float32 kernel
     (1, 1, 8, 40, 5, 3, 16, "f32"),
 ])

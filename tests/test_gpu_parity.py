@@ -94,6 +94,42 @@ def test_prefill_matches_oracle(sata, case):
                                f"{case} {ops} b{b} h{h}")
 
 
+# bf16 shapes without a dedicated kernel: the matrix-core kernel that generates
+# every feature from its monomial (any P >= 2, d_k and d_v up to 64, chunk 64).
+# The cases cover one to five column tiles of 16 (d_v + 1 up to 65), P = 2..7,
+# several feature slices per head, ragged last chunks and single tokens.
+FEATURE_KERNEL_CASES = [
+    # workload, B, H, n, d_k, d_v, P, chunk, dtype
+    (30, 1, 2, 200, 8, 8, 3, 64, "bf16"),
+    (31, 1, 1, 130, 16, 16, 5, 64, "bf16"),
+    (32, 1, 1, 97, 32, 32, 3, 64, "bf16"),
+    (33, 1, 1, 70, 32, 32, 5, 64, "bf16"),
+    (34, 1, 2, 129, 24, 48, 4, 64, "bf16"),
+    (35, 1, 1, 130, 64, 64, 4, 64, "bf16"),
+    (36, 2, 1, 64, 64, 64, 3, 64, "bf16"),
+    (37, 2, 1, 1, 5, 3, 6, 64, "bf16"),
+    # (d_v = 2 rather than 1: a one-element row is a single weighted mean of
+    # N(0,1) values, which lands near zero somewhere in 300 rows, and there a
+    # relative error measures the bf16 rounding of the other terms, not the kernel)
+    (38, 1, 1, 300, 7, 2, 6, 64, "bf16"),
+    (39, 1, 1, 65, 64, 16, 2, 64, "bf16"),
+    (40, 1, 1, 90, 3, 64, 7, 64, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", FEATURE_KERNEL_CASES, ids=lambda c: "w{}_B{}H{}n{}dk{}dv{}P{}C{}_{}".format(*c))
+def test_prefill_generated_features_matches_oracle(sata, case):
+    workload, B, H, n, dk, dv, P, chunk, dtype = case
+    _say(f"prefill (generated features) {case}")
+    ops = operands(sata, dtype, B, H, n, dk, dv, P, chunk)
+    assert ops == "bf16", "expected on the matrix cores"
+    q, k, v, y, S = _run_prefill(sata, *case)
+    for b in range(B):
+        for h in range(H):
+            check_prefill_head(y[b, h], S[b, h], q[b, h], k[b, h], v[b, h], P, ops, dtype, chunk,
+                               f"{case} b{b} h{h}")
+
+
 def test_prefill_empty_sequence_zeroes_state(sata):
     S = torch.full((1, 2, oracle.feature_count(4, 3), 6), 7.0, device="cuda")
     q = torch.empty(1, 2, 0, 4, device="cuda")
