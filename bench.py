@@ -280,8 +280,11 @@ def run_workload(args, sata, torch):
         dec_ms = sum(e[1].elapsed_time(e[2]) for e in events) / args.steps if n_dec else 0.0
         t_total += pre_ms + dec_ms
         flops = prefill_flops_per_head_token(d, d, Pw, CHUNK) * Bw * Hw * n
-        mfma = sata.prefill_operands(tdt, Bw, Hw, n, d, d, Pw, CHUNK) == "bf16"  # on the matrix cores
-        peak = PEAK_BF16_TFLOPS if mfma else PEAK_F32_TFLOPS
+        # on the matrix cores: bf16 operands (bf16 peak), or float32 inputs as
+        # split bf16 pairs (priced at the float32 matrix peak of their dtype)
+        ops = sata.prefill_operands(tdt, Bw, Hw, n, d, d, Pw, CHUNK)
+        mfma = ops in ("bf16", "split")
+        peak = PEAK_BF16_TFLOPS if ops == "bf16" else PEAK_F32_TFLOPS
         ach = flops / (pre_ms * 1e-3) / 1e12
         roof_pre = {"kernel": "sata_prefill (all launches of one call)", "bound": "mfma" if mfma else "alu",
                     "achieved": ach, "peak": peak, "unit": "TFLOP/s", "frac": ach / peak, "traffic": None,

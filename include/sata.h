@@ -143,14 +143,25 @@ sata_status sata_backward(const void* q, const void* k, const void* v, const voi
                           int B, int H, int n, int d_k, int d_v, int P, int chunk,
                           void* dq, void* dk, void* dv, void* stream);
 
+/* Operand precision of the state contractions (sata_prefill_operands). */
+typedef enum {
+  SATA_OPERANDS_F32 = 0,   /* every product formed in float32 (vector units)              */
+  SATA_OPERANDS_BF16 = 1,  /* bfloat16 operands, float32 accumulation (matrix cores)       */
+  SATA_OPERANDS_SPLIT = 2  /* float32 operands carried as bfloat16 pairs hi + lo, each
+                              product as hi*hi + hi*lo + lo*hi (matrix cores)             */
+} sata_operands;
+
 /* Precision of the operands of the state contractions that sata_prefill uses
- * for these arguments (host only, no GPU use; same validation as sata_prefill):
- * *operands = SATA_BF16 when they run on the matrix cores with bfloat16
- * operands and float32 accumulation, SATA_F32 when every product is formed in
- * float32.  The state is float32 in both cases; callers use this to know the
- * accuracy to expect (about 2^-8 relative per term with bfloat16 operands). */
+ * for these arguments (host only, no GPU use; same validation as sata_prefill).
+ * The state is float32 in every case; callers use this to know the accuracy
+ * to expect: about 2^-8 relative per term with bfloat16 operands, 2^-16 with
+ * split operands, 2^-24 with float32 ones.  bfloat16 inputs take bfloat16
+ * operands, float32 inputs split operands, where a matrix-core kernel covers
+ * the shape (chunk 64 and d_k, d_v <= 64 with P >= 2; other chunks only for
+ * the tuned bfloat16 P = 4, d in {16, 32} kernels); float32 arithmetic
+ * otherwise. */
 sata_status sata_prefill_operands(sata_dtype dt, int B, int H, int n, int d_k, int d_v, int P, int chunk,
-                                  sata_dtype* operands);
+                                  sata_operands* operands);
 
 /* One decode step for every (b, h) (App. A2, the linear recurrences for Z_{p,T}
  * and S_{p,T}, then the readout at q_T): S += phi(k) (x) [v, 1], then

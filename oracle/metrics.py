@@ -92,12 +92,17 @@ def state_tol(operands: str, n: int, chunk: int, P: int, steps: int = 0) -> floa
     float32 roundings.  A chunk's sum of `chunk` terms and the n/chunk additions
     of chunk sums into the running state each add at most one float32 rounding
     of a partial sum, which is itself at most S_abs; so does each decode step.
-    The bound allows twice the first-order term."""
+    Split operands carry each float32 operand a as hi = bf16(a) and
+    lo = bf16(a - hi), so |a - hi - lo| <= u^2 |a|, and form a product as
+    hi*hi + hi*lo + lo*hi, leaving out |lo_a lo_b| <= u^2 |a b|: a term is off
+    by at most 3u^2 of its size.  The bound allows twice the first-order term."""
     if n + steps <= 0:
         return 0.0
     accum = (chunk + math.ceil(n / chunk) + steps + 4 * P) * _U32
     if operands == "bf16":
         return 4.0 * _UBF16 + 2.0 * accum
+    if operands == "split":
+        return 6.0 * _UBF16 ** 2 + 2.0 * accum
     if operands == "f32":
         return 2.0 * accum
     raise ValueError(f"unknown operand precision {operands!r}")
@@ -105,11 +110,12 @@ def state_tol(operands: str, n: int, chunk: int, P: int, steps: int = 0) -> floa
 
 def y_tol(operands: str, out_dtype: str) -> float:
     """Row tolerance for y: 2e-2 when the contractions take bfloat16 operands;
-    with float32 arithmetic, 1e-4 for a float32 output and 2^-8 for a bfloat16
-    one (whose storage rounding is up to 2^-9 per element)."""
+    with float32 (or split: float32 carried as bfloat16 pairs) arithmetic, 1e-4
+    for a float32 output and 2^-8 for a bfloat16 one (whose storage rounding is
+    up to 2^-9 per element)."""
     if operands == "bf16":
         return TOL_BF16
-    if operands != "f32":
+    if operands not in ("f32", "split"):
         raise ValueError(f"unknown operand precision {operands!r}")
     return TOL_F32 if out_dtype == "f32" else TOL_F32_ARITH_BF16_OUT
 

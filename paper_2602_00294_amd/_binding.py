@@ -177,8 +177,9 @@ def feature_map(x, P: int):
 
 
 def prefill_operands(dtype, B: int, H: int, n: int, d_k: int, d_v: int, P: int, chunk: int = 64) -> str:
-    """Operand precision ('bf16' or 'f32') of the state contractions that
-    prefill uses for these arguments (host only)."""
+    """Operand precision of the state contractions that prefill uses for these
+    arguments (host only): 'bf16' (bfloat16 operands), 'split' (float32
+    operands as bfloat16 hi + lo pairs, three products each) or 'f32'."""
     torch = _torch()
     code = {torch.float32: SATA_F32, torch.bfloat16: SATA_BF16}.get(dtype)
     if code is None:
@@ -186,7 +187,7 @@ def prefill_operands(dtype, B: int, H: int, n: int, d_k: int, d_v: int, P: int, 
     out = ctypes.c_int(-1)
     _check(load_library().sata_prefill_operands(code, B, H, n, d_k, d_v, P, chunk, ctypes.byref(out)),
            "sata_prefill_operands")
-    return "bf16" if out.value == SATA_BF16 else "f32"
+    return {0: "f32", 1: "bf16", 2: "split"}[out.value]
 
 
 def prefill(q, k, v, P: int, chunk: int = 64, want_state: bool = True, y=None, S=None):

@@ -1,10 +1,16 @@
-// Matrix-core causal prefill for bfloat16 inputs and any (d_k, d_v <= 64, P):
-// the state contractions of the chunked scan (App. A2),
+// Matrix-core causal prefill for any (d_k, d_v <= 64, P >= 2) with 64-token
+// chunks: the state contractions of the chunked scan (App. A2),
 //     O_c = phi(Q_c) S_{c-1},      S_c = S_{c-1} + phi(K_c)^T [V_c | 1],
 // on v_mfma_f32_16x16x32_bf16 with the state in float32 accumulator registers
 // for the whole sequence, every feature generated directly from its monomial.
 //
-// Work split.  A workgroup (8 or 4 waves) owns a contiguous range of features of
+// Operands.  bfloat16 inputs: each operand is rounded to bfloat16 once.
+// float32 inputs ("split" operands): each operand a is carried as a pair of
+// bfloat16 numbers hi = bf16(a), lo = bf16(a - hi), which holds a to about
+// 2^-16 of its size, and each product as hi*hi + hi*lo + lo*hi (the dropped
+// lo*lo is of the same order), three matrix-core products in place of one.
+//
+// Work split.  A workgroup of 8 waves owns a contiguous range of features of
 // one head ("slice") and all d_v + 1 columns (padded to NCT tiles of 16); each
 // wave owns FT tiles of 16 features of it.  Per 64-token chunk a wave walks its
 // features in blocks of 32 (two tiles):
@@ -12,13 +18,15 @@
 //     one token per lane (each feature is a weight times a product of
 //     coordinates; consecutive features that differ in their last index only
 //     reuse the product of the others);
-//   * read out: O[token tile][column tile] += Phi_Q(16 x 32) * bf16(S block);
+//   * read out: O[token tile][column tile] += Phi_Q(16 x 32) * S block;
 //   * update:   S tile += Phi_K^T(16 x 32 tokens) * [V | 1](32 x 16).
-// The readout uses the state before the chunk's update, so the inter-chunk
-// term is exactly phi(Q_c) S_{c-1}.  The waves' partial readouts are added in
-// wave order through LDS and the slice's partial row written per token; the
-// float32 prefill's finalize kernel adds the slices' partials in slice order,
-// adds the intra-chunk term and divides.
+// With split operands the query features are generated, read out, and their
+// LDS block then reused for the key features (so the two halves of a pair
+// fit).  The readout uses the state before the chunk's update, so the
+// inter-chunk term is exactly phi(Q_c) S_{c-1}.  The waves' partial readouts
+// are added in wave order through LDS and the slice's partial row written per
+// token; a second kernel adds the slices' partials in slice order and the
+// float32 prefill's finalize kernel adds the intra-chunk term and divides.
 //
 // Operand layouts (16 x 16 x 32 bf16): A lane l holds row l % 16 and K entries
 // 8 (l / 16) .. +7; B lane l holds column l % 16 and the same K entries; the
@@ -47,10 +55,13 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned short u16;
 
 constexpr int kCh = 64;        // tokens per chunk
+constexpr int kNW = 8;         // waves per workgroup
 constexpr int kQS = 40;        // bf16 per token row of a wave's Phi_Q block (32 + 8 pad)
 constexpr int kKS = 72;        // bf16 per feature row of a wave's Phi_K^T block (64 + 8 pad)
 constexpr int kVS = 72;        // bf16 per column row of V^T
-constexpr int kWaveLds = kCh * kQS * 2 + 32 * kKS * 2;  // bytes of one wave's feature blocks
+constexpr int kRS = 20;        // floats per (wave, column) row of the reduction buffer (16 tokens + 4 pad)
+constexpr int kQPlane = kCh * kQS * 2;  // bytes of one Phi_Q plane
+constexpr int kKPlane = 32 * kKS * 2;   // bytes of one Phi_K^T plane
 
 __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
   bf16x2 v;
@@ -63,6 +74,9 @@ __device__ __forceinline__ u16 bf16_bits(float x) {
   const __bf16 b = (__bf16)x;
   return __builtin_bit_cast(u16, b);
 }
+
+// The part of x that bf16(x) leaves out.
+__device__ __forceinline__ float bf16_rest(float x) { return x - (float)(__bf16)x; }
 
 __device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -87,49 +101,58 @@ __host__ __device__ constexpr int x_stride(int d) { return (d + 1) | 1; }
 constexpr int kXMax = 65;  // x_stride(64): the key rows start at a fixed offset
 
 // LDS map (bytes): region A = x~ of the chunk's queries and keys (float32
-// [64][XS] each, 64 * kXMax floats apart) and V^T (bf16 [NCT*16][kVS]); the cross-wave reduction
-// buffer (float32 [NW][16][NCT*16]) reuses region A after the generation;
-// then the waves' feature blocks.
+// [64][XS] each, 64 * kXMax floats apart) and V^T (PL planes of bf16
+// [NCT*16][kVS]), then the waves' feature blocks (Phi_Q and Phi_K^T; with
+// split operands one hi and one lo plane, shared by the two).  After a chunk's
+// matrix work the reduction buffer (float32 [NW][NCT*16][kRS] per token tile,
+// TP tiles at a time) reuses all of it.
+template <int NCT, bool X3>
 struct FeatLds {
-  int xs, nct, nw, ft;
-  __host__ __device__ int region_a() const {
-    const int x = 2 * kCh * kXMax * 4 + nct * 16 * kVS * 2;
-    const int r = nw * 16 * nct * 16 * 4;
-    return ((x > r ? x : r) + 15) & ~15;
-  }
-  __host__ __device__ int bytes() const { return region_a() + nw * kWaveLds; }
+  static constexpr int kPl = X3 ? 2 : 1;
+  static constexpr int kWave = X3 ? 2 * kQPlane : kQPlane + kKPlane;
+  static constexpr int kRegionA = (2 * kCh * kXMax * 4 + kPl * NCT * 16 * kVS * 2 + 15) & ~15;
+  static constexpr int kRedTile = kNW * NCT * 16 * kRS * 4;
+  static constexpr int kAll = kRegionA + kNW * kWave;
+  static constexpr int kTP = 4 * kRedTile <= kAll ? 4 : 2 * kRedTile <= kAll ? 2 : 1;  // reduction tiles per pass
+  static constexpr int kBytes = kAll > kRedTile ? kAll : kRedTile;
 };
 
-// NW waves per workgroup, FT tiles of 16 features per wave, NCT column tiles.
-template <int NCT, int FT, int NW>
-__global__ void __launch_bounds__(NW * 64, 1)
-prefill_feat_main(const u16* __restrict__ q, const u16* __restrict__ k, const u16* __restrict__ v,
+// FT tiles of 16 features per wave, NCT column tiles; X3: float32 inputs, split operands.
+template <int NCT, int FT, bool X3>
+__global__ void __launch_bounds__(kNW * 64, 1)
+prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, const void* __restrict__ v_,
                   const uint64_t* __restrict__ packed, const uint32_t* __restrict__ gen, int64_t D,
                   float* __restrict__ S_state, float* __restrict__ part, int BH, int n, int dk, int dv, int seg0,
                   int seg_len, int first_seg, int qg) {
   static_assert(FT % 2 == 0, "feature tiles come in blocks of two");
-  static_assert(NW * FT * 16 <= kTablePad, "a slice may end past the last feature by less than the table's padding");
+  static_assert(kNW * FT * 16 <= kTablePad, "a slice may end past the last feature by less than the table's padding");
+  using T = std::conditional_t<X3, float, u16>;
+  using L = FeatLds<NCT, X3>;
+  constexpr int kEV = 16 / sizeof(T);  // elements per 16-byte vector
+  constexpr int kVPlane = NCT * 16 * kVS;  // bf16 per V^T plane
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int E = dv + 1;
   const int XS = x_stride(dk);
-  const FeatLds L{XS, NCT, NW, FT};
-  char* const ra = smem;
-  float* const xq = (float*)ra;
+  float* const xq = (float*)smem;
   float* const xk = xq + kCh * kXMax;
-  u16* const vt = (u16*)(xk + kCh * XS);
-  float* const red = (float*)ra;  // after the generation of a chunk
+  u16* const vt = (u16*)(xk + kCh * kXMax);
+  float* const red = (float*)smem;  // after the matrix work of a chunk
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int l15 = lane & 15;
   const int h4 = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  u16* const phq = (u16*)(ra + L.region_a() + wave * kWaveLds);  // [64][kQS]
-  u16* const phk = phq + kCh * kQS;                                 // [32][kKS]
+  char* const wl = smem + L::kRegionA + wave * L::kWave;
+  u16* const phq = (u16*)wl;                                  // [64][kQS] (hi plane; lo plane next)
+  u16* const phk = (u16*)(X3 ? wl : wl + kQPlane);            // [32][kKS] (hi plane; lo plane next)
+  constexpr int kQLo = X3 ? kQPlane / 2 : 0;                  // u16 from a hi plane to its lo plane
+  constexpr int kKLo = X3 ? kQPlane / 2 : 0;
   const int slice = blockIdx.x;
   const int64_t bh = blockIdx.y;
-  const int fslice = slice * NW * FT * 16;   // (features fit 32 bits: D <= 2^26)
+  const int fslice = slice * kNW * FT * 16;  // (features fit 32 bits: D <= 2^26)
   const int Di = (int)D;
   const int fw0 = fslice + wave * FT * 16;  // this wave's first feature
+
   // the state tiles: S[t][j] holds features fw0 + 16 t + 4 h4 + r, column 16 j + l15
   f32x4 S[FT][NCT];
 #pragma unroll
@@ -148,101 +171,111 @@ prefill_feat_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
       S[t][j] = s;
     }
 
-  const u16* const qh = q + bh * (int64_t)qg * n * dk;
-  const u16* const kh = k + bh * (int64_t)n * dk;
-  const u16* const vh = v + bh * (int64_t)n * dv;
+  const T* const qh = (const T*)q_ + bh * (int64_t)qg * n * dk;
+  const T* const kh = (const T*)k_ + bh * (int64_t)n * dk;
+  const T* const vh = (const T*)v_ + bh * (int64_t)n * dv;
   const int seg_end = min(n, seg0 + seg_len);
   // The next chunk's q, k and v are fetched into registers (16-byte vectors of
-  // eight bf16 of one row) while the current chunk is processed, when every
-  // row of the head starts 16-byte aligned; otherwise element by element.
-  constexpr int kVec = kCh * 64 / 8 / (NW * 64);  // vectors per thread and tensor at d = 64
-  const bool vec = dk % 8 == 0 && dv % 8 == 0 && (((uintptr_t)qh | (uintptr_t)kh | (uintptr_t)vh) & 15) == 0;
+  // one row) while the current chunk is processed, when every row of the head
+  // starts 16-byte aligned; otherwise element by element.
+  constexpr int kVec = kCh * 64 / kEV / (kNW * 64);  // vectors per thread and tensor at d = 64
+  const bool vec = dk % kEV == 0 && dv % kEV == 0 && (((uintptr_t)qh | (uintptr_t)kh | (uintptr_t)vh) & 15) == 0;
   uint4 rq[kVec], rk[kVec], rv[kVec];
   auto fetch = [&](int c0) {
     const int cn = min(kCh, n - c0);
 #pragma unroll
     for (int i = 0; i < kVec; ++i) {
-      const int idx = tid + i * NW * 64;
+      const int idx = tid + i * kNW * 64;
       const uint4 z = {0u, 0u, 0u, 0u};
       rq[i] = z;
       rk[i] = z;
       rv[i] = z;
-      if (idx < cn * dk / 8) {
-        rq[i] = *(const uint4*)(qh + (int64_t)c0 * dk + 8 * idx);
-        rk[i] = *(const uint4*)(kh + (int64_t)c0 * dk + 8 * idx);
+      if (idx < cn * dk / kEV) {
+        rq[i] = *(const uint4*)(qh + (int64_t)c0 * dk + kEV * idx);
+        rk[i] = *(const uint4*)(kh + (int64_t)c0 * dk + kEV * idx);
       }
-      if (idx < cn * dv / 8) rv[i] = *(const uint4*)(vh + (int64_t)c0 * dv + 8 * idx);
+      if (idx < cn * dv / kEV) rv[i] = *(const uint4*)(vh + (int64_t)c0 * dv + kEV * idx);
+    }
+  };
+  // element j of a 16-byte vector (j a constant after unrolling)
+  auto elem = [](const uint4& w, int j) -> T {
+    const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+    if constexpr (X3) return __uint_as_float(u[j]);
+    else return (u16)(j & 1 ? u[j >> 1] >> 16 : u[j >> 1] & 0xffffu);
+  };
+  auto elem_f32 = [&](const uint4& w, int j) -> float {
+    if constexpr (X3) return elem(w, j);
+    else return __uint_as_float((uint32_t)elem(w, j) << 16);
+  };
+  auto to_f32 = [](T x) -> float {
+    if constexpr (X3) return x;
+    else return __uint_as_float((uint32_t)x << 16);
+  };
+  // V^T entry (column c, token t) of value x: both planes with split operands
+  auto put_v = [&](int c, int t, T x) {
+    if constexpr (X3) {
+      vt[c * kVS + t] = bf16_bits(x);
+      vt[kVPlane + c * kVS + t] = bf16_bits(bf16_rest(x));
+    } else {
+      vt[c * kVS + t] = x;
     }
   };
   if (vec) fetch(seg0);
   for (int t0 = seg0; t0 < seg_end; t0 += kCh) {
     const int cn = min(kCh, n - t0);
-    __syncthreads();  // the previous chunk's reduction has read region A
+    __syncthreads();  // the previous chunk's reduction has read its buffer
     if (vec) {
       // rows past the sequence arrive as zeros, so their features are finite
       // and their V^T columns (normaliser included) are zero
 #pragma unroll
       for (int i = 0; i < kVec; ++i) {
-        const int idx = tid + i * NW * 64;
-        if (idx < kCh * dk / 8) {
-          const int t = idx / (dk / 8);
-          const int c = 8 * (idx - t * (dk / 8));
-          const uint32_t w[4] = {rq[i].x, rq[i].y, rq[i].z, rq[i].w};
-          const uint32_t u[4] = {rk[i].x, rk[i].y, rk[i].z, rk[i].w};
+        const int idx = tid + i * kNW * 64;
+        if (idx < kCh * dk / kEV) {
+          const int t = idx / (dk / kEV);
+          const int c = kEV * (idx - t * (dk / kEV));
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            xq[t * XS + c + 2 * j] = __uint_as_float(w[j] << 16);
-            xq[t * XS + c + 2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);
-            xk[t * XS + c + 2 * j] = __uint_as_float(u[j] << 16);
-            xk[t * XS + c + 2 * j + 1] = __uint_as_float(u[j] & 0xffff0000u);
+          for (int j = 0; j < kEV; ++j) {
+            xq[t * XS + c + j] = elem_f32(rq[i], j);
+            xk[t * XS + c + j] = elem_f32(rk[i], j);
           }
         }
-        if (idx < kCh * dv / 8) {
-          const int t = idx / (dv / 8);
-          const int c = 8 * (idx - t * (dv / 8));
-          const uint32_t w[4] = {rv[i].x, rv[i].y, rv[i].z, rv[i].w};
+        if (idx < kCh * dv / kEV) {
+          const int t = idx / (dv / kEV);
+          const int c = kEV * (idx - t * (dv / kEV));
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            vt[(c + 2 * j) * kVS + t] = (u16)(w[j] & 0xffff);
-            vt[(c + 2 * j + 1) * kVS + t] = (u16)(w[j] >> 16);
-          }
+          for (int j = 0; j < kEV; ++j) put_v(c + j, t, elem(rv[i], j));
         }
-      }
-      for (int t = tid; t < kCh; t += NW * 64) {
-        xq[t * XS + dk] = 1.f;
-        xk[t * XS + dk] = 1.f;
-      }
-      for (int i = tid; i < (NCT * 16 - dv) * kCh; i += NW * 64) {
-        const int c = dv + i / kCh;
-        const int t = i - (c - dv) * kCh;
-        vt[c * kVS + t] = (c == dv && t < cn) ? (u16)0x3f80 : (u16)0;
       }
       if (t0 + kCh < seg_end) fetch(t0 + kCh);
     } else {
-      for (int i = tid; i < kCh * dk; i += NW * 64) {
+      for (int i = tid; i < kCh * dk; i += kNW * 64) {
         const int t = i / dk;
         const int c = i - t * dk;
         float a = 0.f, b = 0.f;
         if (t < cn) {
-          a = __uint_as_float((uint32_t)qh[(int64_t)(t0 + t) * dk + c] << 16);
-          b = __uint_as_float((uint32_t)kh[(int64_t)(t0 + t) * dk + c] << 16);
+          a = to_f32(qh[(int64_t)(t0 + t) * dk + c]);
+          b = to_f32(kh[(int64_t)(t0 + t) * dk + c]);
         }
         xq[t * XS + c] = a;
         xk[t * XS + c] = b;
       }
-      for (int t = tid; t < kCh; t += NW * 64) {
-        xq[t * XS + dk] = 1.f;
-        xk[t * XS + dk] = 1.f;
-      }
-      // V^T with the constant-1 normaliser column; tokens past the sequence and
-      // padding columns are zero, so they add nothing to the state
-      for (int i = tid; i < NCT * 16 * kCh; i += NW * 64) {
+      for (int i = tid; i < dv * kCh; i += kNW * 64) {
         const int c = i / kCh;
         const int t = i - c * kCh;
-        u16 b = 0;
-        if (t < cn) b = (c < dv) ? vh[(int64_t)(t0 + t) * dv + c] : (c == dv ? (u16)0x3f80 : (u16)0);
-        vt[c * kVS + t] = b;
+        put_v(c, t, t < cn ? vh[(int64_t)(t0 + t) * dv + c] : (T)0);
       }
+    }
+    for (int t = tid; t < kCh; t += kNW * 64) {
+      xq[t * XS + dk] = 1.f;
+      xk[t * XS + dk] = 1.f;
+    }
+    // the constant-1 normaliser column (tokens of the sequence only) and the
+    // zero padding columns
+    for (int i = tid; i < (NCT * 16 - dv) * kCh; i += kNW * 64) {
+      const int c = dv + i / kCh;
+      const int t = i - (c - dv) * kCh;
+      vt[c * kVS + t] = (c == dv && t < cn) ? (u16)0x3f80 : (u16)0;
+      if constexpr (X3) vt[kVPlane + c * kVS + t] = 0;
     }
     __syncthreads();
     f32x4 O[4][NCT];
@@ -254,114 +287,177 @@ prefill_feat_main(const u16* __restrict__ q, const u16* __restrict__ k, const u1
     static_for<FT / 2>([&](auto sbc) {
       constexpr int SB = decltype(sbc)::value;
       const int fb0 = fw0 + 32 * SB;
-      asm volatile("" ::: "memory");  // keep each block's table reads inside the block
+      asm volatile("" ::: "memory");  // keep each block's program reads inside the block
       if (fb0 < Di) {  // (wave-uniform)
-      // ---- generation: lane = token; features fb0 .. fb0 + 31 in groups of
-      // eight.  A group's program words (x offset of the last index, flag,
-      // weight) are wave-uniform scalar loads; its last-index coordinates are
-      // read from LDS together; only a flagged feature (a new product of the
-      // other indices: rare, features run through the last index in order)
-      // reads its indices and waits on further coordinate reads.
-      lds_fence();  // the previous block's operand reads have completed
-      {
-        const char* const xqt = (const char*)(xq + lane * XS);
-        const uint2* const gb = (const uint2*)gen + fb0;
-        float pq = 1.f, pk = 1.f;
-        for (int g = 0; g < 4; ++g) {
-          asm volatile("" ::: "memory");
-          uint2 pw[8];
-          float xa[8], xb[8];
+        // ---- generation: lane = token; features fb0 .. fb0 + 31 in groups of
+        // eight.  A group's program words (x offset of the last index, flag,
+        // weight) are wave-uniform scalar loads; its last-index coordinates
+        // are read from LDS together; only a flagged feature (a new product of
+        // the other indices: rare, features run through the last index in
+        // order) reads its indices and waits on further coordinate reads.
+        // W = 0: query features only, 1: key features only, 2: both.
+        auto generate = [&](auto wc) {
+          constexpr int W = decltype(wc)::value;
+          const char* const xqt = (const char*)(xq + lane * XS);
+          const uint2* const gb = (const uint2*)gen + fb0;
+          float pq = 1.f, pk = 1.f;
+          for (int g = 0; g < 4; ++g) {
+            asm volatile("" ::: "memory");
+            uint2 pw[8];
+            float xa[8], xb[8];
 #pragma unroll
-          for (int r = 0; r < 8; ++r) pw[r] = gb[8 * g + r];
+            for (int r = 0; r < 8; ++r) pw[r] = gb[8 * g + r];
 #pragma unroll
-          for (int r = 0; r < 8; ++r) {
-            const uint32_t off = pw[r].x & 0x7fffffffu;
-            xa[r] = *(const float*)(xqt + off);
-            xb[r] = *(const float*)(xqt + off + kCh * kXMax * 4);
-          }
-          float vq[8], vk[8];
+            for (int r = 0; r < 8; ++r) {
+              const uint32_t off = pw[r].x & 0x7fffffffu;
+              if (W != 1) xa[r] = *(const float*)(xqt + off);
+              if (W != 0) xb[r] = *(const float*)(xqt + off + kCh * kXMax * 4);
+            }
+            float vq[8];
 #pragma unroll
-          for (int r = 0; r < 8; ++r) {
-            if (pw[r].x >> 31) {
-              const uint64_t e = packed[fb0 + 8 * g + r];
-              const int p = (int)(e >> 56);
-              pq = 1.f;
-              pk = 1.f;
-              for (int j = 0; j < p - 1; ++j) {
-                const int ix = (int)((e >> (8 * j)) & 0xff);
-                pq *= xq[lane * XS + ix];
-                pk *= xk[lane * XS + ix];
+            for (int r = 0; r < 8; ++r) {
+              if (pw[r].x >> 31) {
+                const uint64_t e = packed[fb0 + 8 * g + r];
+                const int p = (int)(e >> 56);
+                pq = 1.f;
+                pk = 1.f;
+                for (int j = 0; j < p - 1; ++j) {
+                  const int ix = (int)((e >> (8 * j)) & 0xff);
+                  if (W != 1) pq *= xq[lane * XS + ix];
+                  if (W != 0) pk *= xk[lane * XS + ix];
+                }
+              }
+              const float w = __uint_as_float(pw[r].y);
+              if (W != 1) vq[r] = (pq * w) * xa[r];
+              if (W != 0) {
+                const float vk = (pk * w) * xb[r];
+                phk[(8 * g + r) * kKS + lane] = bf16_bits(vk);  // Phi_K^T row, column = token
+                if (X3) phk[kKLo + (8 * g + r) * kKS + lane] = bf16_bits(bf16_rest(vk));
               }
             }
-            const float w = __uint_as_float(pw[r].y);
-            vq[r] = (pq * w) * xa[r];
-            vk[r] = (pk * w) * xb[r];
-            phk[(8 * g + r) * kKS + lane] = bf16_bits(vk[r]);  // Phi_K^T row, column = token
+            if (W != 1) {
+              // Phi_Q: feature 8 g + r = 16 T + 4 hh + r' sits in K slot 8 hh + 4 T + r'
+              const int T = g >> 1, hh = 2 * (g & 1);
+              u16* const row = phq + lane * kQS + 4 * T;
+              *(uint2*)(row + 8 * hh) = uint2{pack2(vq[0], vq[1]), pack2(vq[2], vq[3])};
+              *(uint2*)(row + 8 * (hh + 1)) = uint2{pack2(vq[4], vq[5]), pack2(vq[6], vq[7])};
+              if (X3) {
+                *(uint2*)(row + kQLo + 8 * hh) = uint2{pack2(bf16_rest(vq[0]), bf16_rest(vq[1])),
+                                                       pack2(bf16_rest(vq[2]), bf16_rest(vq[3]))};
+                *(uint2*)(row + kQLo + 8 * (hh + 1)) = uint2{pack2(bf16_rest(vq[4]), bf16_rest(vq[5])),
+                                                             pack2(bf16_rest(vq[6]), bf16_rest(vq[7]))};
+              }
+            }
           }
-          // Phi_Q: feature 8 g + r = 16 T + 4 hh + r' sits in K slot 8 hh + 4 T + r'
-          const int T = g >> 1, hh = 2 * (g & 1);
-          uint2 w2;
-          w2.x = pack2(vq[0], vq[1]);
-          w2.y = pack2(vq[2], vq[3]);
-          *(uint2*)(phq + lane * kQS + 8 * hh + 4 * T) = w2;
-          w2.x = pack2(vq[4], vq[5]);
-          w2.y = pack2(vq[6], vq[7]);
-          *(uint2*)(phq + lane * kQS + 8 * (hh + 1) + 4 * T) = w2;
+        };
+        // ---- readout of the block against the state before this chunk's update
+        auto readout = [&]() {
+          bf16x8 bs[NCT], bl[NCT];
+#pragma unroll
+          for (int j = 0; j < NCT; ++j) {
+            const f32x4 s0 = S[2 * SB][j], s1 = S[2 * SB + 1][j];
+            bs[j] = __builtin_bit_cast(bf16x8, (uint4{pack2(s0[0], s0[1]), pack2(s0[2], s0[3]), pack2(s1[0], s1[1]),
+                                                      pack2(s1[2], s1[3])}));
+            if (X3)
+              bl[j] = __builtin_bit_cast(
+                  bf16x8, (uint4{pack2(bf16_rest(s0[0]), bf16_rest(s0[1])), pack2(bf16_rest(s0[2]), bf16_rest(s0[3])),
+                                 pack2(bf16_rest(s1[0]), bf16_rest(s1[1])), pack2(bf16_rest(s1[2]), bf16_rest(s1[3]))}));
+          }
+#pragma unroll
+          for (int m = 0; m < 4; ++m) {
+            const bf16x8 a = *(const bf16x8*)(phq + (16 * m + l15) * kQS + 8 * h4);
+            if (X3) {
+              const bf16x8 al = *(const bf16x8*)(phq + kQLo + (16 * m + l15) * kQS + 8 * h4);
+#pragma unroll
+              for (int j = 0; j < NCT; ++j) O[m][j] = mfma(al, bs[j], mfma(a, bl[j], mfma(a, bs[j], O[m][j])));
+            } else {
+#pragma unroll
+              for (int j = 0; j < NCT; ++j) O[m][j] = mfma(a, bs[j], O[m][j]);
+            }
+          }
+        };
+        // ---- update: S tile += Phi_K^T [V | 1] (the V^T operands are read
+        // from LDS per block rather than held, to leave registers to the state).
+        // With split operands the chunk's 64 tokens are first summed from zero
+        // and then added to the state, so that each entry takes one float32
+        // rounding per chunk (as the float32 path does) rather than one per
+        // 32-token product.
+        auto update = [&]() {
+          if constexpr (X3) {
+#pragma unroll
+            for (int j = 0; j < NCT; ++j) {
+              f32x4 d0 = {0.f, 0.f, 0.f, 0.f}, d1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+              for (int s = 0; s < 2; ++s) {
+                const bf16x8 a0 = *(const bf16x8*)(phk + l15 * kKS + 32 * s + 8 * h4);
+                const bf16x8 a1 = *(const bf16x8*)(phk + (16 + l15) * kKS + 32 * s + 8 * h4);
+                const bf16x8 a0l = *(const bf16x8*)(phk + kKLo + l15 * kKS + 32 * s + 8 * h4);
+                const bf16x8 a1l = *(const bf16x8*)(phk + kKLo + (16 + l15) * kKS + 32 * s + 8 * h4);
+                const bf16x8 b = *(const bf16x8*)(vt + (16 * j + l15) * kVS + 32 * s + 8 * h4);
+                const bf16x8 bl = *(const bf16x8*)(vt + kVPlane + (16 * j + l15) * kVS + 32 * s + 8 * h4);
+                d0 = mfma(a0l, b, mfma(a0, bl, mfma(a0, b, d0)));
+                d1 = mfma(a1l, b, mfma(a1, bl, mfma(a1, b, d1)));
+              }
+              S[2 * SB][j] += d0;
+              S[2 * SB + 1][j] += d1;
+            }
+          } else {
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {
+              const bf16x8 a0 = *(const bf16x8*)(phk + l15 * kKS + 32 * s + 8 * h4);
+              const bf16x8 a1 = *(const bf16x8*)(phk + (16 + l15) * kKS + 32 * s + 8 * h4);
+#pragma unroll
+              for (int j = 0; j < NCT; ++j) {
+                const bf16x8 b = *(const bf16x8*)(vt + (16 * j + l15) * kVS + 32 * s + 8 * h4);
+                S[2 * SB][j] = mfma(a0, b, S[2 * SB][j]);
+                S[2 * SB + 1][j] = mfma(a1, b, S[2 * SB + 1][j]);
+              }
+            }
+          }
+        };
+        lds_fence();  // the previous block's operand reads have completed
+        if constexpr (X3) {
+          generate(std::integral_constant<int, 0>{});
+          lds_fence();
+          readout();
+          lds_fence();  // its operands are in registers: the block is free for the keys
+          generate(std::integral_constant<int, 1>{});
+          lds_fence();
+          update();
+        } else {
+          generate(std::integral_constant<int, 2>{});
+          lds_fence();
+          readout();
+          update();
         }
-      }
-      lds_fence();
-      // ---- readout of the block against the state before this chunk's update
-      bf16x8 bs[NCT];
-#pragma unroll
-      for (int j = 0; j < NCT; ++j) {
-        uint4 w4;
-        w4.x = pack2(S[2 * SB][j][0], S[2 * SB][j][1]);
-        w4.y = pack2(S[2 * SB][j][2], S[2 * SB][j][3]);
-        w4.z = pack2(S[2 * SB + 1][j][0], S[2 * SB + 1][j][1]);
-        w4.w = pack2(S[2 * SB + 1][j][2], S[2 * SB + 1][j][3]);
-        bs[j] = __builtin_bit_cast(bf16x8, w4);
-      }
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const bf16x8 a = *(const bf16x8*)(phq + (16 * m + l15) * kQS + 8 * h4);
-#pragma unroll
-        for (int j = 0; j < NCT; ++j) O[m][j] = mfma(a, bs[j], O[m][j]);
-      }
-      // ---- update: S tile += Phi_K^T [V | 1] (the V^T operands are read from
-      // LDS per block rather than held, to leave registers to the state)
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        const bf16x8 a0 = *(const bf16x8*)(phk + l15 * kKS + 32 * s + 8 * h4);
-        const bf16x8 a1 = *(const bf16x8*)(phk + (16 + l15) * kKS + 32 * s + 8 * h4);
-#pragma unroll
-        for (int j = 0; j < NCT; ++j) {
-          const bf16x8 b = *(const bf16x8*)(vt + (16 * j + l15) * kVS + 32 * s + 8 * h4);
-          S[2 * SB][j] = mfma(a0, b, S[2 * SB][j]);
-          S[2 * SB + 1][j] = mfma(a1, b, S[2 * SB + 1][j]);
-        }
-      }
       }
     });
 
-    // ---- the waves' partial readouts, added in wave order, one token tile at a time
+    // ---- the waves' partial readouts, added in wave order, TP token tiles at
+    // a time; a lane's four rows of a column are one 16-byte store
     float* const pout = part + (((int64_t)slice * BH + bh) * seg_len + (t0 - seg0)) * E;
     constexpr int RC = NCT * 16;
+    constexpr int TP = L::kTP;
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
-      __syncthreads();  // region A is free (generation done / previous tile read)
+    for (int m0 = 0; m0 < 4; m0 += TP) {
+      __syncthreads();  // the matrix work / the previous pass's sums are done
 #pragma unroll
-      for (int j = 0; j < NCT; ++j)
+      for (int mm = 0; mm < TP; ++mm)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) red[(wave * 16 + 4 * h4 + r) * RC + 16 * j + l15] = O[m][j][r];
+        for (int j = 0; j < NCT; ++j)
+          *(f32x4*)(red + (((mm * kNW + wave) * RC + 16 * j + l15) * kRS + 4 * h4)) = O[m0 + mm][j];
       __syncthreads();
-      for (int i = tid; i < 16 * E; i += NW * 64) {
-        const int rr = i / E;
-        const int c = i - rr * E;
-        float a = 0.f;
+      for (int i = tid; i < TP * 4 * E; i += kNW * 64) {
+        const int mq = i / E;  // token quad of the pass
+        const int c = i - mq * E;
+        const int mm = mq >> 2, tq = mq & 3;
+        f32x4 a = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int w = 0; w < NW; ++w) a += red[(w * 16 + rr) * RC + c];
-        const int t = 16 * m + rr;
-        if (t < cn) pout[(int64_t)t * E + c] = a;
+        for (int w = 0; w < kNW; ++w) a += *(const f32x4*)(red + (((mm * kNW + w) * RC + c) * kRS + 4 * tq));
+        const int t = 16 * (m0 + mm) + 4 * tq;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (t + r < cn) pout[(int64_t)(t + r) * E + c] = a[r];
       }
     }
   }
@@ -396,39 +492,88 @@ __global__ void __launch_bounds__(256) reduce_slices(float* __restrict__ part, i
   part[off] = a;
 }
 
-// Tiles per wave and waves per workgroup for NCT column tiles: the state,
-// the readout sums (4 x NCT tiles) and the value operands fit the registers
-// of two waves per SIMD up to NCT = 3, of one wave per SIMD beyond.
-constexpr int ft_for(int nct) { return nct <= 1 ? 28 : nct == 2 ? 16 : nct == 3 ? 8 : nct == 4 ? 6 : 4; }
-constexpr int nw_for(int nct) { return 8; }
+// Tiles of 16 features per wave for NCT column tiles: the state, the readout
+// sums (4 x NCT tiles) and the generation's registers fit two waves per SIMD.
+constexpr int ft_for(int nct, bool x3) {
+  return x3 ? (nct <= 1 ? 22 : nct == 2 ? 10 : nct == 3 ? 6 : nct == 4 ? 4 : 2)
+            : (nct <= 1 ? 28 : nct == 2 ? 16 : nct == 3 ? 8 : nct == 4 ? 6 : 4);
+}
+// Tiles per wave of the narrow variant: slices of 256 features, for heads
+// whose few features would otherwise leave most waves, or most compute
+// units, without work.
+constexpr int kNarrowFT = 2;
+constexpr int lds_for(int nct, bool x3) {
+  switch (nct) {
+    case 1: return x3 ? FeatLds<1, true>::kBytes : FeatLds<1, false>::kBytes;
+    case 2: return x3 ? FeatLds<2, true>::kBytes : FeatLds<2, false>::kBytes;
+    case 3: return x3 ? FeatLds<3, true>::kBytes : FeatLds<3, false>::kBytes;
+    case 4: return x3 ? FeatLds<4, true>::kBytes : FeatLds<4, false>::kBytes;
+    default: return x3 ? FeatLds<5, true>::kBytes : FeatLds<5, false>::kBytes;
+  }
+}
 
-template <int NCT>
-hipError_t launch_main(const u16* q, const u16* k, const u16* v, const DevTable& t, float* S_state, float* part,
+template <int NCT, bool X3, int FT>
+hipError_t launch_main(const void* q, const void* k, const void* v, const DevTable& t, float* S_state, float* part,
                        int BH, int n, int dk, int dv, int seg0, int seg_len, bool first, int nslices, int qg,
                        hipStream_t s) {
-  constexpr int FT = ft_for(NCT), NW = nw_for(NCT);
-  const FeatLds L{x_stride(dk), NCT, NW, FT};
-  auto kern = prefill_feat_main<NCT, FT, NW>;
-  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, L.bytes());
+  constexpr int bytes = FeatLds<NCT, X3>::kBytes;
+  static_assert(bytes <= 160 * 1024, "LDS of one workgroup");
+  auto kern = prefill_feat_main<NCT, FT, X3>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3((unsigned)nslices, (unsigned)BH), dim3(NW * 64), (size_t)L.bytes(), s, q, k, v,
+  hipLaunchKernelGGL(kern, dim3((unsigned)nslices, (unsigned)BH), dim3(kNW * 64), (size_t)bytes, s, q, k, v,
                      t.packed, t.gen, t.D, S_state, part, BH, n, dk, dv, seg0, seg_len, first ? 1 : 0, qg);
   return hipGetLastError();
 }
 
+template <int NCT, bool X3>
+hipError_t launch_main_ft(bool narrow, const void* q, const void* k, const void* v, const DevTable& t,
+                          float* S_state, float* part, int BH, int n, int dk, int dv, int seg0, int seg_len,
+                          bool first, int nslices, int qg, hipStream_t s) {
+  if (narrow)
+    return launch_main<NCT, X3, kNarrowFT>(q, k, v, t, S_state, part, BH, n, dk, dv, seg0, seg_len, first, nslices,
+                                           qg, s);
+  return launch_main<NCT, X3, ft_for(NCT, X3)>(q, k, v, t, S_state, part, BH, n, dk, dv, seg0, seg_len, first,
+                                               nslices, qg, s);
+}
+
+template <bool X3>
+hipError_t launch_main_nct(const FeatPrefillPlan& p, const void* q, const void* k, const void* v, const DevTable& t,
+                           float* S_state, float* part, int BH, int n, int dk, int dv, int seg0, bool first, int qg,
+                           hipStream_t s) {
+  switch (p.nct) {
+    case 1: return launch_main_ft<1, X3>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
+    case 2: return launch_main_ft<2, X3>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
+    case 3: return launch_main_ft<3, X3>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
+    case 4: return launch_main_ft<4, X3>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
+    default: return launch_main_ft<5, X3>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
+  }
+}
+
 }  // namespace
 
-bool plan_prefill_feat(int64_t D, int BH, int n, int dk, int dv, int P, int chunk, size_t max_ws_bytes,
+bool plan_prefill_feat(int64_t D, int BH, int n, int dk, int dv, int P, int chunk, bool split, size_t max_ws_bytes,
                        FeatPrefillPlan* plan) {
   if (chunk != kCh || P < 2 || dk > 64 || dv > 64 || n < 1) return false;
   const int E = dv + 1;
   const int nct = (E + 15) / 16;
-  const int fslice = nw_for(nct) * ft_for(nct) * 16;
+  // Wide or narrow slices, by a simple model of the time per chunk: rounds of
+  // one workgroup per compute unit (256) times the features of the busiest
+  // wave plus a fixed share (loading the chunk, the reduction) worth about 32
+  // features.  Narrow slices win where the wide ones leave compute units or
+  // waves idle (few heads, few features).
+  auto cost = [&](int ft) {
+    const int64_t fs = (int64_t)kNW * ft * 16;
+    const int64_t rounds = ((D + fs - 1) / fs * BH + 255) / 256;
+    return rounds * (32 + std::min<int64_t>((int64_t)ft * 16, D));
+  };
+  plan->narrow = cost(kNarrowFT) < cost(ft_for(nct, split));
+  const int64_t wide = kNW * ft_for(nct, split) * 16, narrow = kNW * kNarrowFT * 16;
+  const int64_t fslice = plan->narrow ? narrow : wide;
   plan->nct = nct;
+  plan->split = split;
   plan->nslices = (int)((D + fslice - 1) / fslice);
-  const FeatLds L{x_stride(dk), nct, nw_for(nct), ft_for(nct)};
-  plan->lds_main = (size_t)L.bytes();
-  if (plan->lds_main > 160 * 1024) return false;
+  plan->lds_main = (size_t)lds_for(nct, split);
   const size_t per_token = sizeof(float) * (size_t)plan->nslices * BH * E;
   int64_t seg = (int64_t)(max_ws_bytes / per_token) / kCh * kCh;
   if (seg < kCh) seg = kCh;
@@ -441,19 +586,12 @@ bool plan_prefill_feat(int64_t D, int BH, int n, int dk, int dv, int P, int chun
 hipError_t launch_prefill_feat(const void* q, const void* k, const void* v, void* y, int BH, int n, int dk, int dv,
                                int P, const DevTable& t, const FeatPrefillPlan& plan, float* S_state, float* partial,
                                hipStream_t s, int qg) {
-  const u16* qq = (const u16*)q;
-  const u16* kk = (const u16*)k;
-  const u16* vv = (const u16*)v;
   for (int seg0 = 0; seg0 < n; seg0 += plan.seg_len) {
     const bool first = seg0 == 0;
-    hipError_t e;
-    switch (plan.nct) {
-      case 1: e = launch_main<1>(qq, kk, vv, t, S_state, partial, BH, n, dk, dv, seg0, plan.seg_len, first, plan.nslices, qg, s); break;
-      case 2: e = launch_main<2>(qq, kk, vv, t, S_state, partial, BH, n, dk, dv, seg0, plan.seg_len, first, plan.nslices, qg, s); break;
-      case 3: e = launch_main<3>(qq, kk, vv, t, S_state, partial, BH, n, dk, dv, seg0, plan.seg_len, first, plan.nslices, qg, s); break;
-      case 4: e = launch_main<4>(qq, kk, vv, t, S_state, partial, BH, n, dk, dv, seg0, plan.seg_len, first, plan.nslices, qg, s); break;
-      default: e = launch_main<5>(qq, kk, vv, t, S_state, partial, BH, n, dk, dv, seg0, plan.seg_len, first, plan.nslices, qg, s); break;
-    }
+    hipError_t e = plan.split ? launch_main_nct<true>(plan, q, k, v, t, S_state, partial, BH, n, dk, dv, seg0, first,
+                                                      qg, s)
+                              : launch_main_nct<false>(plan, q, k, v, t, S_state, partial, BH, n, dk, dv, seg0, first,
+                                                       qg, s);
     if (e != hipSuccess) return e;
     int ns = plan.nslices;
     if (ns > 1) {
@@ -464,8 +602,8 @@ hipError_t launch_prefill_feat(const void* q, const void* k, const void* v, void
       if ((e = hipGetLastError()) != hipSuccess) return e;
       ns = 1;
     }
-    e = launch_prefill_generic_finalize(q, k, v, y, true, BH, n, dk, dv, P, kCh, ns, seg0, plan.seg_len, partial, s,
-                                        qg);
+    e = launch_prefill_generic_finalize(q, k, v, y, !plan.split, BH, n, dk, dv, P, kCh, ns, seg0, plan.seg_len,
+                                        partial, s, qg);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

@@ -273,8 +273,8 @@ PrefillPath prefill_path(sata_dtype dt, int BH, int n, int d_k, int d_v, int P, 
   if (dt == SATA_BF16 && sata::plan_prefill_mfma(BH, n, d_k, d_v, P, chunk, &mp)) return PrefillPath::kMfma32;
   if (dt == SATA_BF16 && sata::plan_prefill_blocks(BH, n, d_k, d_v, P, chunk, &mp)) return PrefillPath::kBlocks;
   sata::FeatPrefillPlan fp;
-  if (dt == SATA_BF16 && sata::plan_prefill_feat(sata::feature_count(d_k, P), BH, n, d_k, d_v, P, chunk,
-                                                 kMaxWorkspace, &fp))
+  if (sata::plan_prefill_feat(sata::feature_count(d_k, P), BH, n, d_k, d_v, P, chunk, dt == SATA_F32, kMaxWorkspace,
+                              &fp))
     return PrefillPath::kFeat;
   return PrefillPath::kFloat32;
 }
@@ -315,7 +315,8 @@ sata_status prefill_dispatch(const void* q, const void* k, const void* v, sata_d
   }
 
   sata::FeatPrefillPlan fp;
-  if (path == PrefillPath::kFeat && sata::plan_prefill_feat(D, BH, n, d_k, d_v, P, chunk, kMaxWorkspace, &fp)) {
+  if (path == PrefillPath::kFeat &&
+      sata::plan_prefill_feat(D, BH, n, d_k, d_v, P, chunk, dt == SATA_F32, kMaxWorkspace, &fp)) {
     const size_t state_bytes = S_out ? 0 : sizeof(float) * (size_t)BH * D * E;
     void* ws = nullptr;
     if ((st = get_workspace(fp.partial_bytes + state_bytes, s, &ws)) != SATA_OK) return st;
@@ -438,12 +439,15 @@ sata_status sata_feature_map(const void* x, sata_dtype xt, int64_t rows, int d, 
 }
 
 sata_status sata_prefill_operands(sata_dtype dt, int B, int H, int n, int d_k, int d_v, int P, int chunk,
-                                  sata_dtype* operands) {
+                                  sata_operands* operands) {
   if (!operands) return fail(SATA_ERR_INVALID_ARG, "null output pointer");
   int64_t D = 0;
   sata_status st = check_prefill_args(dt, B, H, n, d_k, d_v, P, chunk, &D);
   if (st != SATA_OK) return st;
-  *operands = prefill_path(dt, B * H, n, d_k, d_v, P, chunk) == PrefillPath::kFloat32 ? SATA_F32 : SATA_BF16;
+  if (prefill_path(dt, B * H, n, d_k, d_v, P, chunk) == PrefillPath::kFloat32)
+    *operands = SATA_OPERANDS_F32;
+  else
+    *operands = dt == SATA_BF16 ? SATA_OPERANDS_BF16 : SATA_OPERANDS_SPLIT;
   return ok();
 }
 

@@ -3,9 +3,10 @@ comparisons against the oracle).
 
 Tolerances follow the arithmetic of the path that produced a result, which
 the library reports (``prefill_operands``): rows of y within 2e-2 when the
-state contractions take bfloat16 operands, 1e-4 with float32 arithmetic and a
-float32 output, 2^-8 with float32 arithmetic and a bfloat16 output; states
-element by element within the bound of ``oracle.metrics.state_tol``.
+state contractions take bfloat16 operands, 1e-4 with float32 or split
+(bfloat16 hi + lo pairs) arithmetic and a float32 output, 2^-8 with float32
+arithmetic and a bfloat16 output; states element by element within the bound
+of ``oracle.metrics.state_tol``.
 """
 import numpy as np
 
@@ -32,7 +33,7 @@ def to_host(t):
 
 
 def operands(sata, dtype, B, H, n, dk, dv, P, chunk):
-    """Operand precision ('bf16' or 'f32') of the prefill the library runs for these arguments."""
+    """Operand precision ('bf16', 'split' or 'f32') of the prefill the library runs for these arguments."""
     return sata.prefill_operands(torch_dtype(dtype), B, H, n, dk, dv, P, chunk)
 
 

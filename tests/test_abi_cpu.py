@@ -134,15 +134,25 @@ def test_status_strings(lib):
 
 def test_prefill_operands_query(lib):
     out = ctypes.c_int(-1)
-    # float32 inputs always take float32 products; the benchmark's bf16 shape takes the matrix cores
-    assert lib.sata_prefill_operands(0, 8, 32, 8192, 32, 32, 4, 64, ctypes.byref(out)) == 0 and out.value == 0
+    # chunk 64 and d <= 64: the matrix cores, float32 inputs as split (hi + lo
+    # bfloat16) operands; other chunks of float32 inputs: float32 products
+    assert lib.sata_prefill_operands(0, 8, 32, 8192, 32, 32, 4, 64, ctypes.byref(out)) == 0 and out.value == 2
     assert lib.sata_prefill_operands(1, 8, 32, 8192, 32, 32, 4, 64, ctypes.byref(out)) == 0 and out.value == 1
+    assert lib.sata_prefill_operands(0, 1, 64, 65536, 16, 16, 6, 64, ctypes.byref(out)) == 0 and out.value == 2
+    assert lib.sata_prefill_operands(0, 1, 1, 100, 8, 8, 4, 32, ctypes.byref(out)) == 0 and out.value == 0
+    assert lib.sata_prefill_operands(1, 1, 1, 100, 8, 8, 4, 32, ctypes.byref(out)) == 0 and out.value == 0
+    assert lib.sata_prefill_operands(1, 1, 1, 100, 8, 8, 3, 64, ctypes.byref(out)) == 0 and out.value == 1
+    # d_k above 64, and P = 1 (a single feature): float32 products
+    assert lib.sata_prefill_operands(1, 1, 1, 100, 65, 8, 2, 64, ctypes.byref(out)) == 0 and out.value == 0
+    assert lib.sata_prefill_operands(1, 1, 1, 100, 8, 8, 1, 64, ctypes.byref(out)) == 0 and out.value == 0
     # the same validation as the prefill itself
     assert lib.sata_prefill_operands(1, 1, 1, 8, 32, 32, 4, 48, ctypes.byref(out)) == -2
     assert lib.sata_prefill_operands(7, 1, 1, 8, 32, 32, 4, 64, ctypes.byref(out)) == -1
     assert lib.sata_prefill_operands(1, 1, 1, 8, 32, 32, 4, 64, None) == -1
     torch = pytest.importorskip("torch")
-    assert bnd.prefill_operands(torch.float32, 1, 1, 100, 8, 8, 4, 64) == "f32"
+    assert bnd.prefill_operands(torch.float32, 1, 1, 100, 8, 8, 4, 64) == "split"
+    assert bnd.prefill_operands(torch.float32, 1, 1, 100, 8, 8, 4, 16) == "f32"
+    assert bnd.prefill_operands(torch.bfloat16, 1, 1, 100, 8, 8, 4, 64) == "bf16"
 
 
 class TestBindingRejectsBeforeLaunch:

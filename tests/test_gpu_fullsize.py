@@ -139,11 +139,12 @@ def test_fp32_length_sweep_d16(sata, P):
 
 def test_single_head_d8_all_rows(sata):
     q, k, v = syn.make_qkv(1, 1, 1, 256, 8, 8, "f32")
+    ops = operands(sata, "f32", 1, 1, 256, 8, 8, 4, 64)
     y, S = sata.prefill(*(to_dev(a, "f32") for a in (q, k, v)), 4, 64)
     torch.cuda.synchronize()
     yr, _, kap = oracle.taylor_attention(q[0, 0], k[0, 0], v[0, 0], 4)
-    check_rows(to_host(y)[0, 0], yr, kap, y_tol("f32", "f32"), 4, "d8 n256")
-    check_state(to_host(S)[0, 0], k[0, 0], v[0, 0], 4, "f32", 256, 64, "d8 n256 state")
+    check_rows(to_host(y)[0, 0], yr, kap, y_tol(ops, "f32"), 4, f"d8 n256 ({ops} operands)")
+    check_state(to_host(S)[0, 0], k[0, 0], v[0, 0], 4, ops, 256, 64, "d8 n256 state")
 
 
 def test_reconstruction_error_falls_with_each_term(sata):
@@ -180,6 +181,7 @@ def test_float32_state_beyond_2_pow_24_tokens(sata):
     _say(f"long context n={n}")
     q, k, v = syn.long_head(708, n + steps, d, d)
     dev = [torch.from_numpy(a[:n]).to("cuda").view(1, 1, n, d) for a in (q, k, v)]
+    ops = operands(sata, "f32", 1, 1, n, d, d, P, 64)
     y, S = sata.prefill(*dev, P, 64)
     torch.cuda.synchronize()
     rows = [n - 4096, n - 1]
@@ -192,5 +194,5 @@ def test_float32_state_beyond_2_pow_24_tokens(sata):
     _say("oracle rows")
     yr, _, kap = oracle.taylor_attention_rows(q, k, v, P, rows + list(range(n, n + steps)))
     got = np.concatenate([yg, np.stack(ys)]).astype(np.float64)
-    err, _ = check_rows(got, yr, kap, y_tol("f32", "f32"), P, f"after {n} tokens")
+    err, _ = check_rows(got, yr, kap, y_tol(ops, "f32"), P, f"after {n} tokens ({ops} operands)")
     _say(f"worst row error after {n} tokens: {err:.3e}")

@@ -94,8 +94,9 @@ def test_prefill_matches_oracle(sata, case):
                                f"{case} {ops} b{b} h{h}")
 
 
-# bf16 shapes without a dedicated kernel: the matrix-core kernel that generates
-# every feature from its monomial (any P >= 2, d_k and d_v up to 64, chunk 64).
+# Shapes without a dedicated kernel: the matrix-core kernel that generates
+# every feature from its monomial (any P >= 2, d_k and d_v up to 64, chunk 64;
+# bf16 inputs as bf16 operands, float32 inputs as split hi + lo operands).
 # The cases cover one to five column tiles of 16 (d_v + 1 up to 65), P = 2..7,
 # several feature slices per head, ragged last chunks and single tokens.
 FEATURE_KERNEL_CASES = [
@@ -114,6 +115,16 @@ FEATURE_KERNEL_CASES = [
     (38, 1, 1, 300, 7, 2, 6, 64, "bf16"),
     (39, 1, 1, 65, 64, 16, 2, 64, "bf16"),
     (40, 1, 1, 90, 3, 64, 7, 64, "bf16"),
+    # float32 inputs: split operands (16-byte vector loads where d_k and d_v
+    # are multiples of 4, element loads otherwise)
+    (41, 1, 2, 200, 8, 8, 3, 64, "f32"),
+    (42, 1, 1, 130, 16, 16, 5, 64, "f32"),
+    (43, 1, 1, 97, 32, 32, 4, 64, "f32"),
+    (44, 1, 2, 129, 24, 48, 4, 64, "f32"),
+    (45, 1, 1, 130, 64, 64, 3, 64, "f32"),
+    (46, 2, 1, 1, 5, 3, 6, 64, "f32"),
+    (47, 1, 1, 300, 7, 2, 6, 64, "f32"),
+    (48, 1, 1, 90, 3, 64, 7, 64, "f32"),
 ]
 
 
@@ -122,12 +133,35 @@ def test_prefill_generated_features_matches_oracle(sata, case):
     workload, B, H, n, dk, dv, P, chunk, dtype = case
     _say(f"prefill (generated features) {case}")
     ops = operands(sata, dtype, B, H, n, dk, dv, P, chunk)
-    assert ops == "bf16", "expected on the matrix cores"
+    assert ops == ("bf16" if dtype == "bf16" else "split"), "expected on the matrix cores"
     q, k, v, y, S = _run_prefill(sata, *case)
     for b in range(B):
         for h in range(H):
             check_prefill_head(y[b, h], S[b, h], q[b, h], k[b, h], v[b, h], P, ops, dtype, chunk,
                                f"{case} b{b} h{h}")
+
+
+# Many heads and features: the wide slices (more feature tiles per wave) that
+# the kernel takes when they still give at least two workgroups per compute
+# unit; one case per column-tile count and input type, sampled heads.
+WIDE_CASES = [
+    # workload, d_k, d_v, P
+    (50, 32, 8, 4), (51, 16, 16, 5), (52, 32, 40, 4), (53, 24, 48, 4), (54, 16, 64, 4),
+]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("case", WIDE_CASES, ids=lambda c: "w{}_dk{}dv{}P{}".format(*c))
+def test_prefill_generated_features_wide_slices(sata, case, dtype):
+    workload, dk, dv, P = case
+    B, H, n = 1, 256, 40
+    _say(f"prefill (generated features, wide slices) {case} {dtype}")
+    ops = operands(sata, dtype, B, H, n, dk, dv, P, 64)
+    assert ops == ("bf16" if dtype == "bf16" else "split")
+    q, k, v, y, S = _run_prefill(sata, workload, B, H, n, dk, dv, P, 64, dtype)
+    for h in (0, 85, 170, 255):
+        check_prefill_head(y[0, h], S[0, h] if h in (0, 255) else None, q[0, h], k[0, h], v[0, h], P, ops, dtype, 64,
+                           f"{case} {dtype} h{h}")
 
 
 def test_prefill_empty_sequence_zeroes_state(sata):
@@ -149,15 +183,23 @@ def test_prefill_deterministic(sata):
 
 
 def test_prefill_chunk_invariance(sata):
-    """The chunk size changes only the rounding: float32 path, d = 8."""
+    """The chunk size changes only the rounding: float32 inputs, d = 8.  Chunks
+    16, 32 and 128 run in float32 arithmetic; chunk 64 on the matrix cores with
+    split operands, held to that arithmetic's bounds against chunk 16."""
     q, k, v = syn.make_qkv(21, 1, 1, 300, 8, 8, "f32")
-    outs = [sata.prefill(*(to_dev(a, "f32") for a in (q, k, v)), 4, c) for c in (16, 32, 64, 128)]
+    chunks = (16, 32, 64, 128)
+    ops = {c: operands(sata, "f32", 1, 1, 300, 8, 8, 4, c) for c in chunks}
+    assert ops == {16: "f32", 32: "f32", 64: "split", 128: "f32"}
+    outs = {c: sata.prefill(*(to_dev(a, "f32") for a in (q, k, v)), 4, c) for c in chunks}
     torch.cuda.synchronize()
-    y0, S0 = to_host(outs[0][0]), to_host(outs[0][1])
+    y0, S0 = to_host(outs[16][0]), to_host(outs[16][1])
     S_abs = oracle.state_abs_ref(k[0, 0], v[0, 0], 4)
-    for y, S in outs[1:]:
-        assert max_row_rel_error(to_host(y)[0, 0], y0[0, 0])[0] < 1e-5
-        check_state_against(to_host(S)[0, 0], S0[0, 0], S_abs, 2e-5, "chunk invariance")
+    for c in (32, 128):
+        assert max_row_rel_error(to_host(outs[c][0])[0, 0], y0[0, 0])[0] < 1e-5
+        check_state_against(to_host(outs[c][1])[0, 0], S0[0, 0], S_abs, 2e-5, f"chunk {c}")
+    assert max_row_rel_error(to_host(outs[64][0])[0, 0], y0[0, 0])[0] < y_tol("split", "f32")
+    check_state_against(to_host(outs[64][1])[0, 0], S0[0, 0], S_abs,
+                        oracle.state_tol("split", 300, 64, 4) + oracle.state_tol("f32", 300, 16, 4), "chunk 64")
 
 
 @pytest.mark.parametrize("d", [16, 32])

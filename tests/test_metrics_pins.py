@@ -64,9 +64,11 @@ def test_tolerances():
     assert me.state_tol("f32", 256, 64, 4) == 2 * (64 + 4 + 16) * u32
     assert me.state_tol("f32", 256, 64, 4, steps=10) == 2 * (64 + 4 + 10 + 16) * u32
     assert me.state_tol("bf16", 8192, 64, 4) == 4 * ubf + 2 * (64 + 128 + 16) * u32
+    assert me.state_tol("split", 65536, 64, 6) == 6 * ubf ** 2 + 2 * (64 + 1024 + 24) * u32
     assert me.state_tol("f32", 0, 64, 4) == 0.0
     assert me.y_tol("bf16", "bf16") == 2e-2 and me.y_tol("bf16", "f32") == 2e-2
     assert me.y_tol("f32", "f32") == 1e-4 and me.y_tol("f32", "bf16") == 2.0 ** -8
+    assert me.y_tol("split", "f32") == 1e-4
     with pytest.raises(ValueError):
         me.state_tol("f16", 8, 8, 2)
 
