@@ -93,14 +93,15 @@ sata_status sata_feature_map(const void* x, sata_dtype xt, int64_t rows, int d, 
  *          token n-1, ready for sata_decode_step.
  * chunk: tokens per scan block, one of 16, 32, 64, 128.  The result does not
  * depend on it beyond float rounding.  n = 0 writes a zero S_out and no y.
- * Intermediate arithmetic is float32 (bf16 operands with float32 accumulation
- * on the matrix cores for bf16 inputs); the state is always float32.
- * Workspace: the matrix-core paths (bf16, P = 4, d_k = d_v in {16, 32}) keep
- * every token's float32 partial readouts in the library's workspace (576 bytes
- * per head and token at d_k = 32, chunk 64); the float32 path works in
- * segments of at most 512 MB.  SATA_ERR_HIP if the workspace cannot be
- * allocated; SATA_ERR_UNSUPPORTED if a chunk's tiles do not fit on chip (for
- * example d_k = 255 with chunk 64). */
+ * Intermediate arithmetic is float32 or on the matrix cores with float32
+ * accumulation (sata_prefill_operands tells which); the state is always float32.
+ * Workspace: the tuned matrix-core kernels (bf16, P = 4, d_k = d_v in
+ * {16, 32}) keep every token's float32 partial readouts (576 bytes per head
+ * and token at d_k = 32, chunk 64) and serve a call only while those fit in
+ * 4 GB; longer calls, and every other shape, work in segments whose partial
+ * sums take at most 512 MB, so the workspace stays bounded for any n.
+ * SATA_ERR_HIP if the workspace cannot be allocated; SATA_ERR_UNSUPPORTED if
+ * a chunk's tiles do not fit on chip (for example d_k = 255 with chunk 64). */
 sata_status sata_prefill(const void* q, const void* k, const void* v, sata_dtype dt,
                          int B, int H, int n, int d_k, int d_v, int P, int chunk,
                          void* y, float* S_out, void* stream);

@@ -67,8 +67,11 @@ std::map<int, DeviceCache> g_devices;
 constexpr int64_t kMaxFeatures = (int64_t)1 << 26;
 // Upper bound on B*H (one grid dimension per head).
 constexpr int kMaxHeads = 65535;
-// Upper bound on the partial-readout workspace one call may use.
+// Upper bound on the partial-readout workspace of one segment of a call.
 constexpr size_t kMaxWorkspace = (size_t)512 << 20;
+// The tuned matrix-core kernels hold the partial readouts of the whole call;
+// beyond this much the call takes the segmented kernels instead.
+constexpr size_t kMaxWholeCallWorkspace = (size_t)4 << 30;
 // The flat decode kernel (the one that takes residuals) serves d_v up to this.
 constexpr int kMaxCompensatedDv = 127;
 
@@ -270,8 +273,12 @@ enum class PrefillPath { kMfma32, kBlocks, kFeat, kFloat32 };
 // The kernel family that serves a validated prefill request.
 PrefillPath prefill_path(sata_dtype dt, int BH, int n, int d_k, int d_v, int P, int chunk) {
   sata::MfmaPrefillPlan mp;
-  if (dt == SATA_BF16 && sata::plan_prefill_mfma(BH, n, d_k, d_v, P, chunk, &mp)) return PrefillPath::kMfma32;
-  if (dt == SATA_BF16 && sata::plan_prefill_blocks(BH, n, d_k, d_v, P, chunk, &mp)) return PrefillPath::kBlocks;
+  if (dt == SATA_BF16 && sata::plan_prefill_mfma(BH, n, d_k, d_v, P, chunk, &mp) &&
+      mp.workspace_bytes <= kMaxWholeCallWorkspace)
+    return PrefillPath::kMfma32;
+  if (dt == SATA_BF16 && sata::plan_prefill_blocks(BH, n, d_k, d_v, P, chunk, &mp) &&
+      mp.workspace_bytes <= kMaxWholeCallWorkspace)
+    return PrefillPath::kBlocks;
   sata::FeatPrefillPlan fp;
   if (sata::plan_prefill_feat(sata::feature_count(d_k, P), BH, n, d_k, d_v, P, chunk, dt == SATA_F32, kMaxWorkspace,
                               &fp))

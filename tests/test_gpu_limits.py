@@ -104,3 +104,26 @@ def test_most_heads(sata):
     S = _prefill_then_decode(sata, q, k, v, n, P, 64, "bf16", heads)
     del S
     torch.cuda.empty_cache()
+
+
+def test_long_call_keeps_workspace_bounded(sata):
+    """bf16, P = 4, d = 32, chunk 64, 4 heads of 2^21 tokens: the tuned d = 32
+    kernel would hold 576 bytes of partial readouts per head-token (4.8 GB), so
+    the call takes the segmented matrix-core kernel (at most 512 MB of partial
+    sums per segment).  Sampled rows of two heads against the oracle."""
+    H, n, d, P = 4, 1 << 21, 32, 4
+    _say(f"long bf16 call H={H} n={n}: generate inputs")
+    heads = [tuple(syn.round_to_bf16(a) for a in syn.long_head(720 + h, n, d, d)) for h in range(H)]
+    qd, kd, vd = (torch.stack([torch.from_numpy(hd[i]) for hd in heads]).view(1, H, n, d).to("cuda")
+                  .to(torch.bfloat16) for i in range(3))
+    assert operands(sata, "bf16", 1, H, n, d, d, P, 64) == "bf16"
+    _say("prefill")
+    y, _ = sata.prefill(qd, kd, vd, P, 64, want_state=False)
+    torch.cuda.synchronize()
+    rows = [0, 63, 64, 4097, n // 3, n - 65, n - 1]
+    for h in (0, H - 1):
+        _say(f"oracle rows head {h}")
+        q, k, v = (a.astype(np.float64) for a in heads[h])
+        yr, _, kap = oracle.taylor_attention_rows(q, k, v, P, rows)
+        got = y[0, h, rows].float().cpu().numpy().astype(np.float64)
+        check_rows(got, yr, kap, y_tol("bf16", "bf16"), P, f"long call head {h}")
