@@ -69,6 +69,10 @@ constexpr int64_t kMaxFeatures = (int64_t)1 << 26;
 constexpr int kMaxHeads = 65535;
 // Upper bound on the partial-readout workspace of one segment of a call.
 constexpr size_t kMaxWorkspace = (size_t)512 << 20;
+// The same for the generated-feature kernel, whose segments each store and
+// reload the whole state (at d = 64 a 4096-token call of 16 heads is one
+// segment).
+constexpr size_t kMaxFeatWorkspace = (size_t)2 << 30;
 // The tuned matrix-core kernels hold the partial readouts of the whole call;
 // beyond this much the call takes the segmented kernels instead.
 constexpr size_t kMaxWholeCallWorkspace = (size_t)4 << 30;
@@ -280,7 +284,7 @@ PrefillPath prefill_path(sata_dtype dt, int BH, int n, int d_k, int d_v, int P, 
       mp.workspace_bytes <= kMaxWholeCallWorkspace)
     return PrefillPath::kBlocks;
   sata::FeatPrefillPlan fp;
-  if (sata::plan_prefill_feat(sata::feature_count(d_k, P), BH, n, d_k, d_v, P, chunk, dt == SATA_F32, kMaxWorkspace,
+  if (sata::plan_prefill_feat(sata::feature_count(d_k, P), BH, n, d_k, d_v, P, chunk, dt == SATA_F32, kMaxFeatWorkspace,
                               &fp))
     return PrefillPath::kFeat;
   return PrefillPath::kFloat32;
@@ -323,7 +327,7 @@ sata_status prefill_dispatch(const void* q, const void* k, const void* v, sata_d
 
   sata::FeatPrefillPlan fp;
   if (path == PrefillPath::kFeat &&
-      sata::plan_prefill_feat(D, BH, n, d_k, d_v, P, chunk, dt == SATA_F32, kMaxWorkspace, &fp)) {
+      sata::plan_prefill_feat(D, BH, n, d_k, d_v, P, chunk, dt == SATA_F32, kMaxFeatWorkspace, &fp)) {
     const size_t state_bytes = S_out ? 0 : sizeof(float) * (size_t)BH * D * E;
     void* ws = nullptr;
     if ((st = get_workspace(fp.partial_bytes + state_bytes, s, &ws)) != SATA_OK) return st;
