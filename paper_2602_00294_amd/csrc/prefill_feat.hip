@@ -309,7 +309,7 @@ prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, cons
             for (int r = 0; r < 8; ++r) pw[r] = gb[8 * g + r];
 #pragma unroll
             for (int r = 0; r < 8; ++r) {
-              const uint32_t off = pw[r].x & 0x7fffffffu;
+              const uint32_t off = pw[r].x & 0x3ffu;
               if (W != 1) xa[r] = *(const float*)(xqt + off);
               if (W != 0) xb[r] = *(const float*)(xqt + off + kCh * kXMax * 4);
             }
@@ -317,18 +317,22 @@ prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, cons
 #pragma unroll
             for (int r = 0; r < 8; ++r) {
               if (pw[r].x >> 31) {
-                // the product of every index but the last: p - 1 <= P - 2
-                // factors, read two at a time (slots past p - 1 read the
-                // coordinate column held at 1)
-                const uint64_t e = packed[fb0 + 8 * g + r];
-                const int p = (int)(e >> 56);
-                auto idx = [&](int j) { return j < p - 1 ? (int)((e >> (8 * j)) & 0xff) : dk; };
-                pq = 1.f;
-                pk = 1.f;
-                for (int j = 0; j < p - 1; j += 2) {
-                  const int i0 = idx(j), i1 = idx(j + 1);
-                  if (W != 1) pq *= xq[lane * XS + i0] * xq[lane * XS + i1];
-                  if (W != 0) pk *= xk[lane * XS + i0] * xk[lane * XS + i1];
+                // the product of every index but the last: the first two
+                // come with the program word (the column held at 1 where the
+                // feature has fewer), any further ones from the packed entry,
+                // read two at a time
+                const int a0 = (int)((pw[r].x >> 10) & 0xff), a1 = (int)((pw[r].x >> 18) & 0xff);
+                if (W != 1) pq = xq[lane * XS + a0] * xq[lane * XS + a1];
+                if (W != 0) pk = xk[lane * XS + a0] * xk[lane * XS + a1];
+                if ((pw[r].x >> 30) & 1) {
+                  const uint64_t e = packed[fb0 + 8 * g + r];
+                  const int p = (int)(e >> 56);
+                  auto idx = [&](int j) { return j < p - 1 ? (int)((e >> (8 * j)) & 0xff) : dk; };
+                  for (int j = 2; j < p - 1; j += 2) {
+                    const int i0 = idx(j), i1 = idx(j + 1);
+                    if (W != 1) pq *= xq[lane * XS + i0] * xq[lane * XS + i1];
+                    if (W != 0) pk *= xk[lane * XS + i0] * xk[lane * XS + i1];
+                  }
                 }
               }
               const float w = __uint_as_float(pw[r].y);

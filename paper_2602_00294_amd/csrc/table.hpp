@@ -105,30 +105,37 @@ inline FeatureTable build_table(int d, int P) {
 // Generation program of the matrix-core prefill that computes features from
 // their monomials, two 32-bit words per feature (followed by `pad` entries
 // for slices that run past the last feature):
-//   word 0: byte offset 4 i_p of the feature's last index in a float32 row of
-//           coordinates (degree 0 and padding: 4 d, a column that holds 1),
-//           bit 31 set where the product of the other indices must be formed
-//           anew: at every multiple of `block` features and wherever the
-//           degree or an index other than the last changes;
+//   word 0: bits 0-9: byte offset 4 i_p of the feature's last index in a
+//           float32 row of coordinates (degree 0 and padding: 4 d, a column
+//           that holds 1); bits 10-17 and 18-25: the first two of the other
+//           indices (d where the feature has fewer); bit 30: it has more than
+//           two other indices (the rest are read from the packed entry);
+//           bit 31: the product of the other indices must be formed anew, at
+//           every multiple of `block` features and wherever the degree or an
+//           index other than the last changes;
 //   word 1: the feature weight (0 for padding).
 // Features run through their last index in order (for_each_tuple), so the
 // product of the others is shared by runs of up to d consecutive features.
 inline std::vector<uint32_t> build_gen_program(const FeatureTable& t, int pad, int block) {
   std::vector<uint32_t> g(2 * ((size_t)t.D + pad));
+  const uint32_t d = (uint32_t)t.d;
   uint64_t prev_key = ~(uint64_t)0;
   for (int64_t f = 0; f < t.D + pad; ++f) {
-    uint32_t off = 4u * (uint32_t)t.d, w = 0;
+    uint32_t off = 4u * d, a0 = d, a1 = d, more = 0, w = 0;
     uint64_t key = ~(uint64_t)0 - 1;  // padding: one key for all
     if (f < t.D) {
       const uint64_t e = t.packed[(size_t)f];
       const int p = packed_degree(e);
       if (p > 0) off = 4u * (uint32_t)packed_index(e, p - 1);
+      if (p > 1) a0 = (uint32_t)packed_index(e, 0);
+      if (p > 2) a1 = (uint32_t)packed_index(e, 1);
+      more = p > 3 ? 1u : 0u;
       key = p > 0 ? e & ~((uint64_t)0xff << (8 * (p - 1))) : e;
       std::memcpy(&w, &t.weight[(size_t)f], sizeof(w));
     }
     const bool fresh = f % block == 0 || key != prev_key;
     prev_key = key;
-    g[2 * (size_t)f] = off | (fresh ? 0x80000000u : 0u);
+    g[2 * (size_t)f] = off | (a0 << 10) | (a1 << 18) | (more << 30) | (fresh ? 0x80000000u : 0u);
     g[2 * (size_t)f + 1] = w;
   }
   return g;
