@@ -125,7 +125,7 @@ def parse():
     ap.add_argument("--cpu-sample-decode-rows", type=int, default=128)
     ap.add_argument("--workload", default="headline", choices=["headline", "decode_d16", "large_d64", "sweep_d16",
                                                                   "decode_hbm", "error_study", "context_sweep",
-                                                                  "decode_grouped", "backward"])
+                                                                  "decode_grouped", "backward", "feature_map"])
     ap.add_argument("--seq-len", type=int, default=0,
                     help="error_study only: tokens per sequence (default 100000)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -625,6 +625,58 @@ def run_backward(args, sata, torch):
     return line
 
 
+# feature-map workload: (d, P, rows) with about 1-2 GB of float32 features written per call
+FEATURE_MAP_SHAPES = [(16, 4, 262144), (32, 4, 65536), (64, 4, 8192)]
+
+
+def run_feature_map(args, sata, torch):
+    """sata_feature_map alone (Sec. 2.4, "Efficient Computation"): bf16 rows of
+    N(0,1) coordinates expanded to their C(d+3, 3) float32 features.  Bound:
+    HBM, 4 D + 2 d bytes per row (features written, coordinates read)."""
+    import numpy as np
+
+    import sata_synth as syn
+    per = {}
+    t_total = 0.0
+    for (d, P, rows) in FEATURE_MAP_SHAPES:
+        D = feature_count(d, P)
+        x = torch.from_numpy(syn.head_stream(950 + d, 0, 0, syn.TENSOR_Q, (rows, d), "bf16")).to("cuda").to(
+            torch.bfloat16)
+        for _ in range(args.warmup):
+            phi = sata.feature_map(x, P)  # (the output comes from torch's caching allocator)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            phi = sata.feature_map(x, P)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        t_total += ms
+        nbytes = rows * (4 * D + 2 * d)
+        ach = nbytes / (ms * 1e-3) / 1e9
+        r = {"kernel": "feature_map_kernel (one launch per call)", "bound": "hbm", "achieved": ach,
+             "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": ach / PEAK_HBM_GBS, "traffic": None,
+             "work_per_launch": nbytes}
+        per[f"d{d}_P{P}"] = {"rows": rows, "D": D, "ms": ms, "rows_per_s": rows / (ms * 1e-3), "roofline": r}
+        print(f"feature map d={d} P={P} rows={rows}: {ms:.3f} ms, {ach:.0f} GB/s", file=sys.stderr, flush=True)
+        del x, phi
+        torch.cuda.empty_cache()
+    dom = max(per.values(), key=lambda e: e["ms"])["roofline"]
+    total_rows = sum(r for (_, _, r) in FEATURE_MAP_SHAPES)
+    line = {
+        "metric": "prefill tokens/s + decode tokens/s (d_k=32,P=4); % MFMA/HBM roofline",
+        "value": total_rows / (t_total * 1e-3), "unit": "rows/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": t_total, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "feature_map: bf16 rows -> float32 features, " +
+                   ", ".join(f"d={d} P={P} rows={r}" for (d, P, r) in FEATURE_MAP_SHAPES),
+                   "parallelism": "single GPU"},
+        "per_shape": per, "roofline": dom,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def run_context_sweep(args, sata, torch):
     """Prefill of contexts 10^3 ... 10^8 tokens, then decode steps, per head
     size; time and device memory per token.  Inputs: sata_synth.long_head."""
@@ -741,6 +793,9 @@ def main():
         return
     if args.workload == "backward":
         print(json.dumps(run_backward(args, sata, torch)), flush=True)
+        return
+    if args.workload == "feature_map":
+        run_feature_map(args, sata, torch)
         return
     if args.workload == "context_sweep":
         print(json.dumps(run_context_sweep(args, sata, torch)), flush=True)

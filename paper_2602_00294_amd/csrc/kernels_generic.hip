@@ -28,26 +28,6 @@ namespace {
 
 constexpr int kThreads = 256;
 
-// ---------------------------------------------------------------- feature map
-
-constexpr int kFmRows = 16;
-
-template <typename T>
-__global__ void __launch_bounds__(kThreads)
-feature_map_kernel(const T* __restrict__ x, int64_t rows, int d, const uint64_t* __restrict__ packed,
-                   const float* __restrict__ weight, int64_t D, float* __restrict__ phi) {
-  extern __shared__ float xs[];  // [kFmRows][d]
-  const int64_t r0 = (int64_t)blockIdx.x * kFmRows;
-  const int nr = (int)min<int64_t>(kFmRows, rows - r0);
-  for (int i = threadIdx.x; i < nr * d; i += kThreads) xs[i] = to_f32(x[r0 * d + i]);
-  __syncthreads();
-  const int64_t f = (int64_t)blockIdx.y * kThreads + threadIdx.x;
-  if (f >= D) return;
-  const uint64_t pk = packed[f];
-  const float w = weight[f];
-  for (int r = 0; r < nr; ++r) phi[(r0 + r) * D + f] = feature_value(pk, w, xs + r * d);
-}
-
 // ---------------------------------------------------------------- decode step
 
 // Whole-head decode: one workgroup streams all rows of one head's state, so
@@ -730,30 +710,6 @@ hipError_t launch_fill_zero(float* p, int64_t count, hipStream_t s) {
   const int64_t blocks = std::min<int64_t>((count + kThreads - 1) / kThreads, 16384);
   hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, s, p, count);
   return hipGetLastError();
-}
-
-hipError_t launch_feature_map(const void* x, bool bf16, int64_t rows, const DevTable& t, float* phi,
-                              hipStream_t s) {
-  const size_t lds = sizeof(float) * kFmRows * t.d;
-  const int64_t fblocks = (t.D + kThreads - 1) / kThreads;
-  // keep each launch below 2^31 work-items
-  const int64_t max_rb = std::max<int64_t>(1, ((int64_t)1 << 31) / (fblocks * kThreads));
-  const int64_t total_rb = (rows + kFmRows - 1) / kFmRows;
-  for (int64_t rb = 0; rb < total_rb; rb += max_rb) {
-    const int64_t nrb = std::min(max_rb, total_rb - rb);
-    const int64_t r0 = rb * kFmRows;
-    const int64_t nrows = std::min<int64_t>(rows - r0, nrb * kFmRows);
-    dim3 grid((unsigned)nrb, (unsigned)fblocks);
-    if (bf16)
-      hipLaunchKernelGGL(feature_map_kernel<bf16_t>, grid, dim3(kThreads), lds, s,
-                         (const bf16_t*)x + r0 * t.d, nrows, t.d, t.packed, t.weight, t.D, phi + r0 * t.D);
-    else
-      hipLaunchKernelGGL(feature_map_kernel<float>, grid, dim3(kThreads), lds, s,
-                         (const float*)x + r0 * t.d, nrows, t.d, t.packed, t.weight, t.D, phi + r0 * t.D);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
 }
 
 // Share of each (even, odd) pair of decode pieces given to the even one: the

@@ -41,7 +41,10 @@ def _say(msg):
 
 @pytest.mark.parametrize("d,P,rows,dtype", [
     (8, 4, 37, "f32"), (16, 4, 100, "bf16"), (3, 7, 19, "f32"), (32, 4, 65, "bf16"),
-    (1, 1, 5, "f32"), (5, 2, 1, "f32"), (64, 3, 33, "f32")])
+    (1, 1, 5, "f32"), (5, 2, 1, "f32"), (64, 3, 33, "f32"),
+    # the largest d, degrees above 3 over several row blocks, and more rows
+    # than one launch takes (65535 blocks of 32 rows)
+    (255, 2, 40, "bf16"), (16, 6, 3000, "f32"), (1, 2, 2_100_001, "f32")])
 def test_feature_map(sata, d, P, rows, dtype):
     _say(f"feature_map d={d} P={P} rows={rows} {dtype}")
     x = syn.head_stream(100, d, P, 0, (rows, d), dtype)
