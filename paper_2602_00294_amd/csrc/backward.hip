@@ -39,17 +39,26 @@ namespace {
 constexpr int kBwThreads = 256;
 
 // Rows of q, k, [v | 1] and h of one chunk into LDS (zero beyond the sequence).
+// q and k rows are XS floats apart; with XS > dk, column dk holds 1 (the
+// coordinate that degree-0 and lower-degree features read in the generation
+// program).
 template <typename T>
 __device__ void bw_load_chunk(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
                               const float* __restrict__ h, int64_t bh, int n, int t0, int cn, int C, int dk, int dv,
-                              float* xq, float* xk, float* ve, float* hh) {
+                              float* xq, float* xk, float* ve, float* hh, int XS) {
   const int E = dv + 1;
   const int64_t off = (bh * n + t0) * (int64_t)dk;
   for (int i = threadIdx.x; i < C * dk; i += kBwThreads) {
     const int t = i / dk;
-    xq[i] = t < cn ? to_f32(q[off + i]) : 0.0f;
-    xk[i] = t < cn ? to_f32(k[off + i]) : 0.0f;
+    const int c = i - t * dk;
+    xq[t * XS + c] = t < cn ? to_f32(q[off + i]) : 0.0f;
+    xk[t * XS + c] = t < cn ? to_f32(k[off + i]) : 0.0f;
   }
+  if (XS > dk)
+    for (int t = threadIdx.x; t < C; t += kBwThreads) {
+      xq[t * XS + dk] = 1.0f;
+      xk[t * XS + dk] = 1.0f;
+    }
   const int64_t voff = (bh * n + t0) * (int64_t)dv;
   const int64_t hoff = (bh * n + t0) * (int64_t)E;
   for (int i = threadIdx.x; i < C * E; i += kBwThreads) {
@@ -92,16 +101,143 @@ __device__ __forceinline__ void add_feature_gradient(uint64_t pk, float w, float
   }
 }
 
+// out[t * FS + f] = sum_j A[f * E + j] * B[t * E + j] for t < cn, f < fs
+// (A: a feature slice of a state, [fs][E]; B: [C][E] rows, zero past cn),
+// each thread taking 4 tokens x 2 features so that a loaded value serves
+// several products.
+__device__ void bw_rows_dot(const float* A, const float* B, float* out, int fs, int cn, int E, int FS) {
+  const int fp_n = (fs + 1) / 2, tq_n = (cn + 3) / 4;
+  for (int i = threadIdx.x; i < fp_n * tq_n; i += kBwThreads) {
+    const int fp = i % fp_n, tq = i / fp_n;
+    const int f0 = 2 * fp, f1 = min(f0 + 1, fs - 1), t0 = 4 * tq;
+    float acc[4][2] = {{0.f, 0.f}, {0.f, 0.f}, {0.f, 0.f}, {0.f, 0.f}};
+    for (int j = 0; j < E; ++j) {
+      const float a0 = A[f0 * E + j], a1 = A[f1 * E + j];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float b = B[(t0 + r) * E + j];
+        acc[r][0] += a0 * b;
+        acc[r][1] += a1 * b;
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (t0 + r < cn) {
+        out[(t0 + r) * FS + f0] = acc[r][0];
+        if (f0 + 1 < fs) out[(t0 + r) * FS + f0 + 1] = acc[r][1];
+      }
+  }
+}
+
+// S[f * E + j] += sum_{t < cn} F[t * FS + f] * V[t * E + j] for f < fs, j < E,
+// each thread taking 2 features x 4 columns.
+__device__ void bw_accumulate_outer(float* S, const float* F, const float* V, int fs, int cn, int E, int FS) {
+  const int fp_n = (fs + 1) / 2, jq_n = (E + 3) / 4;
+  for (int i = threadIdx.x; i < fp_n * jq_n; i += kBwThreads) {
+    const int fp = i % fp_n, jq = i / fp_n;
+    const int f0 = 2 * fp, f1 = min(f0 + 1, fs - 1), j0 = 4 * jq;
+    float acc[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+    for (int t = 0; t < cn; ++t) {
+      const float a0 = F[t * FS + f0], a1 = F[t * FS + f1];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const float b = V[t * E + min(j0 + c, E - 1)];
+        acc[0][c] += a0 * b;
+        acc[1][c] += a1 * b;
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      if (j0 + c < E) {
+        S[f0 * E + j0 + c] += acc[0][c];
+        if (f0 + 1 < fs) S[f1 * E + j0 + c] += acc[1][c];
+      }
+  }
+}
+
+// out[t * W + j] = sum_{f < fs} U[f * E + j] * F[t * FS + f] for t < cn, j < dv
+// (4 tokens x 2 columns per thread).
+__device__ void bw_cols_dot(const float* U, const float* F, float* out, int fs, int cn, int E, int dv, int FS, int W) {
+  const int jp_n = (dv + 1) / 2, tq_n = (cn + 3) / 4;
+  for (int i = threadIdx.x; i < jp_n * tq_n; i += kBwThreads) {
+    const int jp = i % jp_n, tq = i / jp_n;
+    const int j0 = 2 * jp, j1 = min(j0 + 1, dv - 1), t0 = 4 * tq;
+    float acc[4][2] = {{0.f, 0.f}, {0.f, 0.f}, {0.f, 0.f}, {0.f, 0.f}};
+    for (int f = 0; f < fs; ++f) {
+      const float a0 = U[f * E + j0], a1 = U[f * E + j1];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float b = F[(t0 + r) * FS + f];
+        acc[r][0] += a0 * b;
+        acc[r][1] += a1 * b;
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (t0 + r < cn) {
+        out[(t0 + r) * W + j0] = acc[r][0];
+        if (j0 + 1 < dv) out[(t0 + r) * W + j0 + 1] = acc[r][1];
+      }
+  }
+}
+
+// Value of one feature from its generation-program words g (table.hpp
+// build_gen_program) at the row x (stride with the column d held at 1), the
+// packed entry pk supplying any indices past the first two and the last.
+__device__ __forceinline__ float gen_feature_value(uint2 g, uint64_t pk, const float* x) {
+  float v = __uint_as_float(g.y) * x[(g.x >> 10) & 0xffu] * x[(g.x >> 18) & 0xffu] * x[(g.x & 0x3ffu) >> 2];
+  if ((g.x >> 30) & 1u) {
+    const int p = (int)(pk >> 56);
+    for (int j = 2; j < p - 1; ++j) v *= x[(pk >> (8 * j)) & 0xff];
+  }
+  return v;
+}
+
+// acc[a] += sum over the features f in [lo, hi) of u[f] d phi_f(x) / d x[a],
+// in feature order.  For degree <= 3 (indices a0 <= a1 <= c, the missing ones
+// being the column d, which acc has room for and nobody reads) the last
+// index takes u w x[a0] x[a1] per feature, and the two others take x[a1] and
+// x[a0] times the run sum of u w x[c] over consecutive features that share
+// (a0, a1), added when the run ends; higher degrees take the full product rule.
+__device__ void add_gradient_range(const uint2* gen, const uint64_t* tpk, const float* u, int lo, int hi,
+                                   const float* x, float* acc, int d) {
+  int ca = d, cb = d;
+  float xa = 1.0f, xb = 1.0f, sum = 0.0f;
+  for (int f = lo; f < hi; ++f) {
+    const uint2 g = gen[f];
+    const float uw = u[f] * __uint_as_float(g.y);
+    const int a0 = (int)((g.x >> 10) & 0xffu), a1 = (int)((g.x >> 18) & 0xffu);
+    if ((g.x >> 30) & 1u) {
+      add_feature_gradient(tpk[f], __uint_as_float(g.y), u[f], x, acc);
+      continue;
+    }
+    if (a0 != ca || a1 != cb) {
+      acc[ca] += xb * sum;
+      acc[cb] += xa * sum;
+      sum = 0.0f;
+      ca = a0;
+      cb = a1;
+      xa = x[a0];
+      xb = x[a1];
+    }
+    const int c = (int)((g.x & 0x3ffu) >> 2);
+    acc[c] += uw * xa * xb;
+    sum += uw * x[c];
+  }
+  acc[ca] += xb * sum;
+  acc[cb] += xa * sum;
+}
+
 // Shared LDS layout of the two scan kernels (in floats; the 8-byte table
 // entries first, so they stay aligned):
-//   tpk [FS] (u64) | tw [FS] | Sl [FS][E] state slice | fb [C][FS] feature
-//   values | uu [C][FS] readouts | xq, xk [C][dk] | ve, hh [C][E] |
-//   jq [parts][C][dk] gradient rows
+//   tpk [FS] (u64) | tgen [FS] (program words, 2 x u32) | Sl [FS][E] state
+//   slice | fb [C][FS] feature values | uu [C][FS] readouts | xq, xk
+//   [C][dk+1] | ve, hh [C][E] | jq [parts][C][dk+1] gradient rows
 struct BwLds {
   int FS, C, dk, E, parts;
   __host__ __device__ size_t floats() const {
-    return (size_t)FS * E + 2 * (size_t)C * FS + 2 * (size_t)C * dk + 2 * (size_t)C * E + (size_t)parts * C * dk +
-           3 * (size_t)FS;
+    return (size_t)FS * E + 2 * (size_t)C * FS + 2 * (size_t)C * (dk + 1) + 2 * (size_t)C * E +
+           (size_t)parts * C * (dk + 1) + 4 * (size_t)FS;
   }
 };
 
@@ -109,20 +245,21 @@ struct BwLds {
 template <typename T>
 __global__ void __launch_bounds__(kBwThreads)
 backward_dq_main(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
-                 const float* __restrict__ h, const uint64_t* __restrict__ packed, const float* __restrict__ weight,
+                 const float* __restrict__ h, const uint64_t* __restrict__ packed, const uint32_t* __restrict__ gen,
                  int64_t D, float* __restrict__ S_state, float* __restrict__ part, int BH, int n, int dk, int dv,
                  int C, int FS, int seg0, int seg_len, int first_seg) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
   const int E = dv + 1;
   const int parts = kBwThreads / C;
+  const int XS = dk + 1;
   uint64_t* tpk = (uint64_t*)lds;
-  float* tw = (float*)(tpk + FS);
-  float* Sl = tw + FS;
+  uint2* tgen = (uint2*)(tpk + FS);
+  float* Sl = (float*)(tgen + FS);
   float* fb = Sl + FS * E;
   float* uu = fb + C * FS;
   float* xq = uu + C * FS;
-  float* xk = xq + C * dk;
-  float* ve = xk + C * dk;
+  float* xk = xq + C * XS;
+  float* ve = xk + C * XS;
   float* hh = ve + C * E;
   float* jq = hh + C * E;
   const int s = blockIdx.x;
@@ -134,55 +271,45 @@ backward_dq_main(const T* __restrict__ q, const T* __restrict__ k, const T* __re
   for (int i = tid; i < fs * E; i += kBwThreads) Sl[i] = first_seg ? 0.0f : Sg[i];
   for (int f = tid; f < fs; f += kBwThreads) {
     tpk[f] = packed[f0 + f];
-    tw[f] = weight[f0 + f];
+    tgen[f] = ((const uint2*)gen)[f0 + f];
   }
   const int seg_end = min(n, seg0 + seg_len);
   for (int t0 = seg0; t0 < seg_end; t0 += C) {
     const int cn = min(C, n - t0);
     __syncthreads();
-    bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh);
-    for (int i = tid; i < parts * C * dk; i += kBwThreads) jq[i] = 0.0f;
+    bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh, XS);
+    for (int i = tid; i < parts * C * XS; i += kBwThreads) jq[i] = 0.0f;
     __syncthreads();
     // u_T[f] = S_{c-1}[f, :] . h_T
-    for (int i = tid; i < cn * fs; i += kBwThreads) {
-      const int t = i / fs;
-      const int f = i - t * fs;
-      float a = 0.0f;
-      for (int j = 0; j < E; ++j) a += Sl[f * E + j] * hh[t * E + j];
-      uu[t * FS + f] = a;
-    }
+    bw_rows_dot(Sl, hh, uu, fs, cn, E, FS);
     __syncthreads();
-    // dq_T += sum_f u_T[f] d phi_f(q_T) / d q: thread (part, token) takes the
-    // features f = part mod parts into its own gradient row
+    // dq_T += sum_f u_T[f] d phi_f(q_T) / d q: thread (part, token) takes a
+    // contiguous range of the features into its own gradient row
     {
       const int t = tid % C;
       const int pt = tid / C;
-      if (t < cn) {
-        float* acc = jq + (pt * C + t) * dk;
-        for (int f = pt; f < fs; f += parts) add_feature_gradient(tpk[f], tw[f], uu[t * FS + f], xq + t * dk, acc);
-      }
+      const int per = (fs + parts - 1) / parts;
+      if (t < cn)
+        add_gradient_range(tgen, tpk, uu + t * FS, pt * per, min(fs, (pt + 1) * per), xq + t * XS,
+                           jq + (pt * C + t) * XS, dk);
     }
     __syncthreads();
     float* pout = part + (((int64_t)s * BH + bh) * seg_len + (t0 - seg0)) * dk;
     for (int i = tid; i < cn * dk; i += kBwThreads) {
-      float a = 0.0f;
-      for (int pt = 0; pt < parts; ++pt) a += jq[pt * C * dk + i];
-      pout[i] = a;
+      const int t = i / dk;
+      const int a = i - t * dk;
+      float sum = 0.0f;
+      for (int pt = 0; pt < parts; ++pt) sum += jq[(pt * C + t) * XS + a];
+      pout[i] = sum;
     }
     // S_c = S_{c-1} + phi(K_c)^T [V_c | 1]
     for (int i = tid; i < cn * fs; i += kBwThreads) {
       const int t = i / fs;
       const int f = i - t * fs;
-      fb[t * FS + f] = feature_value(tpk[f], tw[f], xk + t * dk);
+      fb[t * FS + f] = gen_feature_value(tgen[f], tpk[f], xk + t * XS);
     }
     __syncthreads();
-    for (int i = tid; i < fs * E; i += kBwThreads) {
-      const int f = i / E;
-      const int j = i - f * E;
-      float a = 0.0f;
-      for (int t = 0; t < cn; ++t) a += fb[t * FS + f] * ve[t * E + j];
-      Sl[i] += a;
-    }
+    bw_accumulate_outer(Sl, fb, ve, fs, cn, E, FS);
   }
   __syncthreads();
   for (int i = tid; i < fs * E; i += kBwThreads) Sg[i] = Sl[i];
@@ -193,20 +320,21 @@ backward_dq_main(const T* __restrict__ q, const T* __restrict__ k, const T* __re
 template <typename T>
 __global__ void __launch_bounds__(kBwThreads)
 backward_dkv_main(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
-                  const float* __restrict__ h, const uint64_t* __restrict__ packed, const float* __restrict__ weight,
+                  const float* __restrict__ h, const uint64_t* __restrict__ packed, const uint32_t* __restrict__ gen,
                   int64_t D, float* __restrict__ U_state, float* __restrict__ part, int BH, int n, int dk, int dv,
                   int C, int FS, int seg0, int seg_len, int first_seg) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
   const int E = dv + 1;
   const int parts = kBwThreads / C;
+  const int XS = dk + 1;
   uint64_t* tpk = (uint64_t*)lds;
-  float* tw = (float*)(tpk + FS);
-  float* Ul = tw + FS;
+  uint2* tgen = (uint2*)(tpk + FS);
+  float* Ul = (float*)(tgen + FS);
   float* fb = Ul + FS * E;
   float* uu = fb + C * FS;
   float* xq = uu + C * FS;
-  float* xk = xq + C * dk;
-  float* ve = xk + C * dk;
+  float* xk = xq + C * XS;
+  float* ve = xk + C * XS;
   float* hh = ve + C * E;
   float* jq = hh + C * E;
   const int s = blockIdx.x;
@@ -218,33 +346,31 @@ backward_dkv_main(const T* __restrict__ q, const T* __restrict__ k, const T* __r
   for (int i = tid; i < fs * E; i += kBwThreads) Ul[i] = first_seg ? 0.0f : Ug[i];
   for (int f = tid; f < fs; f += kBwThreads) {
     tpk[f] = packed[f0 + f];
-    tw[f] = weight[f0 + f];
+    tgen[f] = ((const uint2*)gen)[f0 + f];
   }
   const int seg_end = min(n, seg0 + seg_len);
   const int PW = dk + dv;  // partial row: dk, then dv
   for (int t0 = seg0 + (seg_end - 1 - seg0) / C * C; t0 >= seg0; t0 -= C) {
     const int cn = min(C, n - t0);
     __syncthreads();
-    bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh);
-    for (int i = tid; i < parts * C * dk; i += kBwThreads) jq[i] = 0.0f;
+    bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh, XS);
+    for (int i = tid; i < parts * C * XS; i += kBwThreads) jq[i] = 0.0f;
     __syncthreads();
     // phi(k_t) and r_t[f] = U[f, :] . [v_t | 1]
     for (int i = tid; i < cn * fs; i += kBwThreads) {
       const int t = i / fs;
       const int f = i - t * fs;
-      fb[t * FS + f] = feature_value(tpk[f], tw[f], xk + t * dk);
-      float a = 0.0f;
-      for (int j = 0; j < E; ++j) a += Ul[f * E + j] * ve[t * E + j];
-      uu[t * FS + f] = a;
+      fb[t * FS + f] = gen_feature_value(tgen[f], tpk[f], xk + t * XS);
     }
+    bw_rows_dot(Ul, ve, uu, fs, cn, E, FS);
     __syncthreads();
     {
       const int t = tid % C;
       const int pt = tid / C;
-      if (t < cn) {
-        float* acc = jq + (pt * C + t) * dk;
-        for (int f = pt; f < fs; f += parts) add_feature_gradient(tpk[f], tw[f], uu[t * FS + f], xk + t * dk, acc);
-      }
+      const int per = (fs + parts - 1) / parts;
+      if (t < cn)
+        add_gradient_range(tgen, tpk, uu + t * FS, pt * per, min(fs, (pt + 1) * per), xk + t * XS,
+                           jq + (pt * C + t) * XS, dk);
     }
     __syncthreads();
     float* pout = part + (((int64_t)s * BH + bh) * seg_len + (t0 - seg0)) * PW;
@@ -252,32 +378,20 @@ backward_dkv_main(const T* __restrict__ q, const T* __restrict__ k, const T* __r
       const int t = i / dk;
       const int a = i - t * dk;
       float sum = 0.0f;
-      for (int pt = 0; pt < parts; ++pt) sum += jq[pt * C * dk + i];
+      for (int pt = 0; pt < parts; ++pt) sum += jq[(pt * C + t) * XS + a];
       pout[t * PW + a] = sum;
     }
     // dv_t[j] = sum_f U[f, j] phi_f(k_t)
-    for (int i = tid; i < cn * dv; i += kBwThreads) {
-      const int t = i / dv;
-      const int j = i - t * dv;
-      float a = 0.0f;
-      for (int f = 0; f < fs; ++f) a += Ul[f * E + j] * fb[t * FS + f];
-      pout[t * PW + dk + j] = a;
-    }
+    bw_cols_dot(Ul, fb, pout + dk, fs, cn, E, dv, FS, PW);
     __syncthreads();
     // U += phi(Q_c)^T H_c
     for (int i = tid; i < cn * fs; i += kBwThreads) {
       const int t = i / fs;
       const int f = i - t * fs;
-      fb[t * FS + f] = feature_value(tpk[f], tw[f], xq + t * dk);
+      fb[t * FS + f] = gen_feature_value(tgen[f], tpk[f], xq + t * XS);
     }
     __syncthreads();
-    for (int i = tid; i < fs * E; i += kBwThreads) {
-      const int f = i / E;
-      const int j = i - f * E;
-      float a = 0.0f;
-      for (int t = 0; t < cn; ++t) a += fb[t * FS + f] * hh[t * E + j];
-      Ul[i] += a;
-    }
+    bw_accumulate_outer(Ul, fb, hh, fs, cn, E, FS);
   }
   __syncthreads();
   for (int i = tid; i < fs * E; i += kBwThreads) Ug[i] = Ul[i];
@@ -387,7 +501,7 @@ backward_dq_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* 
   const int t0 = seg0 + blockIdx.x * C;
   if (t0 >= n) return;
   const int cn = min(C, n - t0);
-  bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh);
+  bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh, dk);
   __syncthreads();
   bw_intra_weights(xq, xk, ve, hh, cn, C, dk, E, P, W, Gm);
   __syncthreads();
@@ -421,7 +535,7 @@ backward_dkv_finalize(const T* __restrict__ q, const T* __restrict__ k, const T*
   const int t0 = seg0 + blockIdx.x * C;
   if (t0 >= n) return;
   const int cn = min(C, n - t0);
-  bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh);
+  bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh, dk);
   __syncthreads();
   bw_intra_weights(xq, xk, ve, hh, cn, C, dk, E, P, W, Gm);
   __syncthreads();
@@ -454,7 +568,7 @@ bool plan_backward(int64_t D, int BH, int n, int dk, int dv, int chunk, size_t m
   BwLds L{0, C, dk, E, kBwThreads / C};
   const size_t budget = 150 * 1024;
   const size_t fixed = sizeof(float) * L.floats();
-  const size_t per_feature = sizeof(float) * ((size_t)E + 2 * (size_t)C + 3);
+  const size_t per_feature = sizeof(float) * ((size_t)E + 2 * (size_t)C + 4);
   if (fixed + 8 * per_feature > budget) return false;
   int64_t fs = (int64_t)((budget - fixed) / per_feature);
   fs = std::min<int64_t>(fs, 512);
@@ -521,7 +635,7 @@ static hipError_t launch_backward_typed(const T* q, const T* k, const T* v, cons
   for (int sg = 0; sg < nseg; ++sg) {
     const int seg0 = sg * plan.seg_len;
     hipLaunchKernelGGL(backward_dq_main<T>, dim3((unsigned)plan.nslices, (unsigned)BH), dim3(kBwThreads),
-                       plan.lds_main, s, q, k, v, h, t.packed, t.weight, t.D, state, partial, BH, n, dk_, dv, C,
+                       plan.lds_main, s, q, k, v, h, t.packed, t.gen, t.D, state, partial, BH, n, dk_, dv, C,
                        plan.fs, seg0, plan.seg_len, sg == 0 ? 1 : 0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const int nchunks = (std::min(plan.seg_len, n - seg0) + C - 1) / C;
@@ -534,7 +648,7 @@ static hipError_t launch_backward_typed(const T* q, const T* k, const T* v, cons
   for (int sg = nseg - 1; sg >= 0; --sg) {
     const int seg0 = sg * plan.seg_len;
     hipLaunchKernelGGL(backward_dkv_main<T>, dim3((unsigned)plan.nslices, (unsigned)BH), dim3(kBwThreads),
-                       plan.lds_main, s, q, k, v, h, t.packed, t.weight, t.D, state, partial, BH, n, dk_, dv, C,
+                       plan.lds_main, s, q, k, v, h, t.packed, t.gen, t.D, state, partial, BH, n, dk_, dv, C,
                        plan.fs, seg0, plan.seg_len, sg == nseg - 1 ? 1 : 0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const int nchunks = (std::min(plan.seg_len, n - seg0) + C - 1) / C;
