@@ -36,7 +36,9 @@ namespace sata {
 
 namespace {
 
-constexpr int kBwThreads = 256;
+constexpr int kBwThreads = 256;      // finalize kernels
+constexpr int kBwScanThreads = 1024;  // scan kernels (four waves per SIMD)
+constexpr int kBwPartThreads = 256;  // threads that take the Jacobian: kBwPartThreads / C feature ranges
 
 // Rows of q, k, [v | 1] and h of one chunk into LDS (zero beyond the sequence).
 // q and k rows are XS floats apart; with XS > dk, column dk holds 1 (the
@@ -48,20 +50,20 @@ __device__ void bw_load_chunk(const T* __restrict__ q, const T* __restrict__ k, 
                               float* xq, float* xk, float* ve, float* hh, int XS) {
   const int E = dv + 1;
   const int64_t off = (bh * n + t0) * (int64_t)dk;
-  for (int i = threadIdx.x; i < C * dk; i += kBwThreads) {
+  for (int i = threadIdx.x; i < C * dk; i += blockDim.x) {
     const int t = i / dk;
     const int c = i - t * dk;
     xq[t * XS + c] = t < cn ? to_f32(q[off + i]) : 0.0f;
     xk[t * XS + c] = t < cn ? to_f32(k[off + i]) : 0.0f;
   }
   if (XS > dk)
-    for (int t = threadIdx.x; t < C; t += kBwThreads) {
+    for (int t = threadIdx.x; t < C; t += blockDim.x) {
       xq[t * XS + dk] = 1.0f;
       xk[t * XS + dk] = 1.0f;
     }
   const int64_t voff = (bh * n + t0) * (int64_t)dv;
   const int64_t hoff = (bh * n + t0) * (int64_t)E;
-  for (int i = threadIdx.x; i < C * E; i += kBwThreads) {
+  for (int i = threadIdx.x; i < C * E; i += blockDim.x) {
     const int t = i / E;
     const int j = i - t * E;
     float val = 0.0f, hv = 0.0f;
@@ -107,7 +109,7 @@ __device__ __forceinline__ void add_feature_gradient(uint64_t pk, float w, float
 // several products.
 __device__ void bw_rows_dot(const float* A, const float* B, float* out, int fs, int cn, int E, int FS) {
   const int fp_n = (fs + 1) / 2, tq_n = (cn + 3) / 4;
-  for (int i = threadIdx.x; i < fp_n * tq_n; i += kBwThreads) {
+  for (int i = threadIdx.x; i < fp_n * tq_n; i += blockDim.x) {
     const int fp = i % fp_n, tq = i / fp_n;
     const int f0 = 2 * fp, f1 = min(f0 + 1, fs - 1), t0 = 4 * tq;
     float acc[4][2] = {{0.f, 0.f}, {0.f, 0.f}, {0.f, 0.f}, {0.f, 0.f}};
@@ -133,7 +135,7 @@ __device__ void bw_rows_dot(const float* A, const float* B, float* out, int fs, 
 // each thread taking 2 features x 4 columns.
 __device__ void bw_accumulate_outer(float* S, const float* F, const float* V, int fs, int cn, int E, int FS) {
   const int fp_n = (fs + 1) / 2, jq_n = (E + 3) / 4;
-  for (int i = threadIdx.x; i < fp_n * jq_n; i += kBwThreads) {
+  for (int i = threadIdx.x; i < fp_n * jq_n; i += blockDim.x) {
     const int fp = i % fp_n, jq = i / fp_n;
     const int f0 = 2 * fp, f1 = min(f0 + 1, fs - 1), j0 = 4 * jq;
     float acc[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
@@ -159,7 +161,7 @@ __device__ void bw_accumulate_outer(float* S, const float* F, const float* V, in
 // (4 tokens x 2 columns per thread).
 __device__ void bw_cols_dot(const float* U, const float* F, float* out, int fs, int cn, int E, int dv, int FS, int W) {
   const int jp_n = (dv + 1) / 2, tq_n = (cn + 3) / 4;
-  for (int i = threadIdx.x; i < jp_n * tq_n; i += kBwThreads) {
+  for (int i = threadIdx.x; i < jp_n * tq_n; i += blockDim.x) {
     const int jp = i % jp_n, tq = i / jp_n;
     const int j0 = 2 * jp, j1 = min(j0 + 1, dv - 1), t0 = 4 * tq;
     float acc[4][2] = {{0.f, 0.f}, {0.f, 0.f}, {0.f, 0.f}, {0.f, 0.f}};
@@ -243,14 +245,14 @@ struct BwLds {
 
 // Pass 2: dL/dq (inter-chunk part), one feature slice of S per workgroup.
 template <typename T>
-__global__ void __launch_bounds__(kBwThreads)
+__global__ void __launch_bounds__(kBwScanThreads)
 backward_dq_main(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
                  const float* __restrict__ h, const uint64_t* __restrict__ packed, const uint32_t* __restrict__ gen,
                  int64_t D, float* __restrict__ S_state, float* __restrict__ part, int BH, int n, int dk, int dv,
                  int C, int FS, int seg0, int seg_len, int first_seg) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
   const int E = dv + 1;
-  const int parts = kBwThreads / C;
+  const int parts = kBwPartThreads / C;
   const int XS = dk + 1;
   uint64_t* tpk = (uint64_t*)lds;
   uint2* tgen = (uint2*)(tpk + FS);
@@ -268,8 +270,8 @@ backward_dq_main(const T* __restrict__ q, const T* __restrict__ k, const T* __re
   const int64_t f0 = (int64_t)s * FS;
   const int fs = (int)min<int64_t>(FS, D - f0);
   float* Sg = S_state + (bh * D + f0) * E;
-  for (int i = tid; i < fs * E; i += kBwThreads) Sl[i] = first_seg ? 0.0f : Sg[i];
-  for (int f = tid; f < fs; f += kBwThreads) {
+  for (int i = tid; i < fs * E; i += blockDim.x) Sl[i] = first_seg ? 0.0f : Sg[i];
+  for (int f = tid; f < fs; f += blockDim.x) {
     tpk[f] = packed[f0 + f];
     tgen[f] = ((const uint2*)gen)[f0 + f];
   }
@@ -278,7 +280,7 @@ backward_dq_main(const T* __restrict__ q, const T* __restrict__ k, const T* __re
     const int cn = min(C, n - t0);
     __syncthreads();
     bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh, XS);
-    for (int i = tid; i < parts * C * XS; i += kBwThreads) jq[i] = 0.0f;
+    for (int i = tid; i < parts * C * XS; i += blockDim.x) jq[i] = 0.0f;
     __syncthreads();
     // u_T[f] = S_{c-1}[f, :] . h_T
     bw_rows_dot(Sl, hh, uu, fs, cn, E, FS);
@@ -289,13 +291,13 @@ backward_dq_main(const T* __restrict__ q, const T* __restrict__ k, const T* __re
       const int t = tid % C;
       const int pt = tid / C;
       const int per = (fs + parts - 1) / parts;
-      if (t < cn)
+      if (t < cn && pt < parts)
         add_gradient_range(tgen, tpk, uu + t * FS, pt * per, min(fs, (pt + 1) * per), xq + t * XS,
                            jq + (pt * C + t) * XS, dk);
     }
     __syncthreads();
     float* pout = part + (((int64_t)s * BH + bh) * seg_len + (t0 - seg0)) * dk;
-    for (int i = tid; i < cn * dk; i += kBwThreads) {
+    for (int i = tid; i < cn * dk; i += blockDim.x) {
       const int t = i / dk;
       const int a = i - t * dk;
       float sum = 0.0f;
@@ -303,7 +305,7 @@ backward_dq_main(const T* __restrict__ q, const T* __restrict__ k, const T* __re
       pout[i] = sum;
     }
     // S_c = S_{c-1} + phi(K_c)^T [V_c | 1]
-    for (int i = tid; i < cn * fs; i += kBwThreads) {
+    for (int i = tid; i < cn * fs; i += blockDim.x) {
       const int t = i / fs;
       const int f = i - t * fs;
       fb[t * FS + f] = gen_feature_value(tgen[f], tpk[f], xk + t * XS);
@@ -312,20 +314,20 @@ backward_dq_main(const T* __restrict__ q, const T* __restrict__ k, const T* __re
     bw_accumulate_outer(Sl, fb, ve, fs, cn, E, FS);
   }
   __syncthreads();
-  for (int i = tid; i < fs * E; i += kBwThreads) Sg[i] = Sl[i];
+  for (int i = tid; i < fs * E; i += blockDim.x) Sg[i] = Sl[i];
 }
 
 // Pass 3: dL/dk and dL/dv (inter-chunk parts), chunks in reverse order, one
 // feature slice of U = sum over later tokens of phi(q_T) (x) h_T per workgroup.
 template <typename T>
-__global__ void __launch_bounds__(kBwThreads)
+__global__ void __launch_bounds__(kBwScanThreads)
 backward_dkv_main(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
                   const float* __restrict__ h, const uint64_t* __restrict__ packed, const uint32_t* __restrict__ gen,
                   int64_t D, float* __restrict__ U_state, float* __restrict__ part, int BH, int n, int dk, int dv,
                   int C, int FS, int seg0, int seg_len, int first_seg) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
   const int E = dv + 1;
-  const int parts = kBwThreads / C;
+  const int parts = kBwPartThreads / C;
   const int XS = dk + 1;
   uint64_t* tpk = (uint64_t*)lds;
   uint2* tgen = (uint2*)(tpk + FS);
@@ -343,8 +345,8 @@ backward_dkv_main(const T* __restrict__ q, const T* __restrict__ k, const T* __r
   const int64_t f0 = (int64_t)s * FS;
   const int fs = (int)min<int64_t>(FS, D - f0);
   float* Ug = U_state + (bh * D + f0) * E;
-  for (int i = tid; i < fs * E; i += kBwThreads) Ul[i] = first_seg ? 0.0f : Ug[i];
-  for (int f = tid; f < fs; f += kBwThreads) {
+  for (int i = tid; i < fs * E; i += blockDim.x) Ul[i] = first_seg ? 0.0f : Ug[i];
+  for (int f = tid; f < fs; f += blockDim.x) {
     tpk[f] = packed[f0 + f];
     tgen[f] = ((const uint2*)gen)[f0 + f];
   }
@@ -354,10 +356,10 @@ backward_dkv_main(const T* __restrict__ q, const T* __restrict__ k, const T* __r
     const int cn = min(C, n - t0);
     __syncthreads();
     bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh, XS);
-    for (int i = tid; i < parts * C * XS; i += kBwThreads) jq[i] = 0.0f;
+    for (int i = tid; i < parts * C * XS; i += blockDim.x) jq[i] = 0.0f;
     __syncthreads();
     // phi(k_t) and r_t[f] = U[f, :] . [v_t | 1]
-    for (int i = tid; i < cn * fs; i += kBwThreads) {
+    for (int i = tid; i < cn * fs; i += blockDim.x) {
       const int t = i / fs;
       const int f = i - t * fs;
       fb[t * FS + f] = gen_feature_value(tgen[f], tpk[f], xk + t * XS);
@@ -368,13 +370,13 @@ backward_dkv_main(const T* __restrict__ q, const T* __restrict__ k, const T* __r
       const int t = tid % C;
       const int pt = tid / C;
       const int per = (fs + parts - 1) / parts;
-      if (t < cn)
+      if (t < cn && pt < parts)
         add_gradient_range(tgen, tpk, uu + t * FS, pt * per, min(fs, (pt + 1) * per), xk + t * XS,
                            jq + (pt * C + t) * XS, dk);
     }
     __syncthreads();
     float* pout = part + (((int64_t)s * BH + bh) * seg_len + (t0 - seg0)) * PW;
-    for (int i = tid; i < cn * dk; i += kBwThreads) {
+    for (int i = tid; i < cn * dk; i += blockDim.x) {
       const int t = i / dk;
       const int a = i - t * dk;
       float sum = 0.0f;
@@ -385,7 +387,7 @@ backward_dkv_main(const T* __restrict__ q, const T* __restrict__ k, const T* __r
     bw_cols_dot(Ul, fb, pout + dk, fs, cn, E, dv, FS, PW);
     __syncthreads();
     // U += phi(Q_c)^T H_c
-    for (int i = tid; i < cn * fs; i += kBwThreads) {
+    for (int i = tid; i < cn * fs; i += blockDim.x) {
       const int t = i / fs;
       const int f = i - t * fs;
       fb[t * FS + f] = gen_feature_value(tgen[f], tpk[f], xq + t * XS);
@@ -394,7 +396,7 @@ backward_dkv_main(const T* __restrict__ q, const T* __restrict__ k, const T* __r
     bw_accumulate_outer(Ul, fb, hh, fs, cn, E, FS);
   }
   __syncthreads();
-  for (int i = tid; i < fs * E; i += kBwThreads) Ug[i] = Ul[i];
+  for (int i = tid; i < fs * E; i += blockDim.x) Ug[i] = Ul[i];
 }
 
 // Intra-chunk weights of one chunk into LDS: for query row r and key column c
@@ -402,7 +404,7 @@ backward_dkv_main(const T* __restrict__ q, const T* __restrict__ k, const T* __r
 __device__ void bw_intra_weights(const float* xq, const float* xk, const float* ve, const float* hh, int cn, int C,
                                  int dk, int E, int P, float* W, float* Gm) {
   const float scale = 1.0f / sqrtf((float)dk);
-  for (int i = threadIdx.x; i < C * C; i += kBwThreads) {
+  for (int i = threadIdx.x; i < C * C; i += blockDim.x) {
     const int r = i / C;
     const int c = i - r * C;
     float w = 0.0f, g = 0.0f;
@@ -440,18 +442,18 @@ backward_h_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* _
   const int tid = threadIdx.x;
   const float scale = 1.0f / sqrtf((float)dk);
   const int64_t off = (bh * n + t0) * (int64_t)dk;
-  for (int i = tid; i < C * dk; i += kBwThreads) {
+  for (int i = tid; i < C * dk; i += blockDim.x) {
     const int t = i / dk;
     xq[i] = t < cn ? to_f32(q[off + i]) : 0.0f;
     xk[i] = t < cn ? to_f32(k[off + i]) : 0.0f;
   }
-  for (int i = tid; i < C * E; i += kBwThreads) {
+  for (int i = tid; i < C * E; i += blockDim.x) {
     const int t = i / E;
     const int j = i - t * E;
     ve[i] = t < cn ? ((j < dv) ? to_f32(v[(bh * n + t0 + t) * (int64_t)dv + j]) : 1.0f) : 0.0f;
   }
   __syncthreads();
-  for (int i = tid; i < C * C; i += kBwThreads) {
+  for (int i = tid; i < C * C; i += blockDim.x) {
     const int r = i / C;
     const int c = i - r * C;
     float w = 0.0f;
@@ -463,7 +465,7 @@ backward_h_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* _
     W[i] = w;
   }
   __syncthreads();
-  for (int o = tid; o < cn * E; o += kBwThreads) {
+  for (int o = tid; o < cn * E; o += blockDim.x) {
     const int r = o / E;
     const int j = o - r * E;
     float acc = 0.0f;
@@ -472,7 +474,7 @@ backward_h_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* _
     O[o] = acc;
   }
   __syncthreads();
-  for (int r = tid; r < cn; r += kBwThreads) {
+  for (int r = tid; r < cn; r += blockDim.x) {
     const float Z = O[r * E + dv];
     const T* g = dy + (bh * n + t0 + r) * (int64_t)dv;
     float gy = 0.0f;
@@ -505,7 +507,7 @@ backward_dq_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* 
   __syncthreads();
   bw_intra_weights(xq, xk, ve, hh, cn, C, dk, E, P, W, Gm);
   __syncthreads();
-  for (int i = threadIdx.x; i < cn * dk; i += kBwThreads) {
+  for (int i = threadIdx.x; i < cn * dk; i += blockDim.x) {
     const int r = i / dk;
     const int a = i - r * dk;
     float acc = 0.0f;
@@ -539,7 +541,7 @@ backward_dkv_finalize(const T* __restrict__ q, const T* __restrict__ k, const T*
   __syncthreads();
   bw_intra_weights(xq, xk, ve, hh, cn, C, dk, E, P, W, Gm);
   __syncthreads();
-  for (int i = threadIdx.x; i < cn * PW; i += kBwThreads) {
+  for (int i = threadIdx.x; i < cn * PW; i += blockDim.x) {
     const int c = i / PW;
     const int a = i - c * PW;
     float acc = 0.0f;
@@ -565,7 +567,7 @@ bool plan_backward(int64_t D, int BH, int n, int dk, int dv, int chunk, size_t m
   if (!plan_prefill_generic(D, BH, n, dk, dv, chunk, max_ws_bytes, fwd)) return false;
   const int E = dv + 1;
   const int C = chunk;
-  BwLds L{0, C, dk, E, kBwThreads / C};
+  BwLds L{0, C, dk, E, kBwPartThreads / C};
   const size_t budget = 150 * 1024;
   const size_t fixed = sizeof(float) * L.floats();
   const size_t per_feature = sizeof(float) * ((size_t)E + 2 * (size_t)C + 4);
@@ -634,7 +636,7 @@ static hipError_t launch_backward_typed(const T* q, const T* k, const T* v, cons
   // pass 2: dq
   for (int sg = 0; sg < nseg; ++sg) {
     const int seg0 = sg * plan.seg_len;
-    hipLaunchKernelGGL(backward_dq_main<T>, dim3((unsigned)plan.nslices, (unsigned)BH), dim3(kBwThreads),
+    hipLaunchKernelGGL(backward_dq_main<T>, dim3((unsigned)plan.nslices, (unsigned)BH), dim3(kBwScanThreads),
                        plan.lds_main, s, q, k, v, h, t.packed, t.gen, t.D, state, partial, BH, n, dk_, dv, C,
                        plan.fs, seg0, plan.seg_len, sg == 0 ? 1 : 0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -647,7 +649,7 @@ static hipError_t launch_backward_typed(const T* q, const T* k, const T* v, cons
   // pass 3: dk, dv, segments from the last
   for (int sg = nseg - 1; sg >= 0; --sg) {
     const int seg0 = sg * plan.seg_len;
-    hipLaunchKernelGGL(backward_dkv_main<T>, dim3((unsigned)plan.nslices, (unsigned)BH), dim3(kBwThreads),
+    hipLaunchKernelGGL(backward_dkv_main<T>, dim3((unsigned)plan.nslices, (unsigned)BH), dim3(kBwScanThreads),
                        plan.lds_main, s, q, k, v, h, t.packed, t.gen, t.D, state, partial, BH, n, dk_, dv, C,
                        plan.fs, seg0, plan.seg_len, sg == nseg - 1 ? 1 : 0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
