@@ -560,11 +560,14 @@ backward_dkv_finalize(const T* __restrict__ q, const T* __restrict__ k, const T*
 
 }  // namespace
 
-bool plan_backward(int64_t D, int BH, int n, int dk, int dv, int chunk, size_t max_ws_bytes, BackwardPlan* plan,
+bool plan_backward(int64_t D, int BH, int n, int dk, int dv, int P, int chunk, size_t max_ws_bytes, BackwardPlan* plan,
                    PrefillGenericPlan* fwd) {
   if (dk > kMaxBackwardDim || dv > kMaxBackwardDim) return false;
   if (chunk != 16 && chunk != 32 && chunk != 64) return false;
   if (!plan_prefill_generic(D, BH, n, dk, dv, chunk, max_ws_bytes, fwd)) return false;
+  // the forward readout of pass 1 on the matrix cores (split operands, so
+  // float32-accurate for both input types) where its kernel covers the shape
+  plan->feat_fwd = plan_prefill_feat(D, BH, std::max(n, 1), dk, dv, P, chunk, true, max_ws_bytes, &plan->feat);
   const int E = dv + 1;
   const int C = chunk;
   BwLds L{0, C, dk, E, kBwPartThreads / C};
@@ -585,14 +588,16 @@ bool plan_backward(int64_t D, int BH, int n, int dk, int dv, int chunk, size_t m
   plan->lds_fin = sizeof(float) * (2 * (size_t)C * dk + 2 * (size_t)C * E + 2 * (size_t)C * C);
   // partial rows per token: the forward readout (E per forward slice), dq (dk),
   // dk and dv (dk + dv) per backward slice
+  const size_t fwd_slices = plan->feat_fwd ? (size_t)plan->feat.nslices : (size_t)fwd->nslices;
   const size_t per_token = sizeof(float) * (size_t)BH *
-                           std::max<size_t>((size_t)fwd->nslices * E, (size_t)plan->nslices * (dk + dv));
+                           std::max<size_t>(fwd_slices * E, (size_t)plan->nslices * (dk + dv));
   int64_t seg = (int64_t)(max_ws_bytes / per_token) / C * C;
   if (seg < C) seg = C;
   const int64_t n_round = ((int64_t)std::max(n, 1) + C - 1) / C * C;
   plan->seg_len = (int)std::min<int64_t>(seg, n_round);
   plan->partial_bytes = per_token * (size_t)plan->seg_len;
   fwd->seg_len = plan->seg_len;
+  plan->feat.seg_len = plan->seg_len;
   plan->h_bytes = sizeof(float) * (size_t)BH * n * E;
   plan->state_bytes = sizeof(float) * (size_t)BH * D * E;
   return true;
@@ -624,13 +629,18 @@ static hipError_t launch_backward_typed(const T* q, const T* k, const T* v, cons
   // pass 1: the forward readout of each segment, then h
   for (int sg = 0; sg < nseg; ++sg) {
     const int seg0 = sg * plan.seg_len;
-    if ((e = launch_prefill_generic_readout(q, k, v, std::is_same<T, bf16_t>::value, BH, n, dk_, dv, C, t, fwd,
-                                            state, partial, seg0, plan.seg_len, sg == 0, s)) != hipSuccess)
-      return e;
+    if (plan.feat_fwd)
+      e = launch_prefill_feat_readout(q, k, v, std::is_same<T, bf16_t>::value, BH, n, dk_, dv, t, plan.feat, state,
+                                      partial, seg0, sg == 0, s);
+    else
+      e = launch_prefill_generic_readout(q, k, v, std::is_same<T, bf16_t>::value, BH, n, dk_, dv, C, t, fwd, state,
+                                         partial, seg0, plan.seg_len, sg == 0, s);
+    if (e != hipSuccess) return e;
     const int nchunks = (std::min(plan.seg_len, n - seg0) + C - 1) / C;
+    // (the matrix-core readout leaves its slices' sum in slice 0)
     hipLaunchKernelGGL(backward_h_finalize<T>, dim3((unsigned)nchunks, (unsigned)BH), dim3(kBwThreads),
-                       plan.lds_h, s, q, k, v, dy, partial, h, BH, n, dk_, dv, P, C, fwd.nslices, seg0,
-                       plan.seg_len);
+                       plan.lds_h, s, q, k, v, dy, partial, h, BH, n, dk_, dv, P, C,
+                       plan.feat_fwd ? 1 : fwd.nslices, seg0, plan.seg_len);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   // pass 2: dq

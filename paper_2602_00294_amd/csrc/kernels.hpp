@@ -103,6 +103,38 @@ hipError_t launch_prefill_generic_finalize(const void* q, const void* k, const v
                                            int n, int dk, int dv, int P, int chunk, int nslices, int seg0,
                                            int seg_len, const float* partial, hipStream_t s, int qg);
 
+// ---- prefill, matrix cores with generated features (prefill_feat.hip) ---------
+// Any d_k, d_v <= 64 and P >= 2 with 64-token chunks; state in accumulators.
+struct FeatPrefillPlan {
+  int nct = 0;             // column tiles of 16 covering d_v + 1
+  bool split = false;      // split operands (hi + lo bfloat16 pairs, three products per product)
+  bool narrow = false;     // slices of 256 features (for few features or few heads)
+  int nslices = 0;         // workgroups per head
+  int seg_len = 0;         // tokens per segment (partial sums of one segment in the workspace)
+  size_t lds_main = 0;
+  size_t partial_bytes = 0;
+};
+
+// True if the kernel covers this shape (chunk 64, P >= 2, d_k, d_v <= 64).
+bool plan_prefill_feat(int64_t D, int BH, int n, int dk, int dv, int P, int chunk, bool split, size_t max_ws_bytes,
+                       FeatPrefillPlan* plan);
+
+// Whole prefill: bf16 inputs with bf16 operands (plan.split false), float32
+// inputs with split operands (plan.split true).  S_state: [BH][D][d_v+1]
+// float32, the state after the call (carried between segments); partial:
+// plan.partial_bytes.  q holds qg query heads per head.
+hipError_t launch_prefill_feat(const void* q, const void* k, const void* v, void* y, int BH, int n, int dk, int dv,
+                               int P, const DevTable& t, const FeatPrefillPlan& plan, float* S_state, float* partial,
+                               hipStream_t s, int qg = 1);
+
+// One segment [seg0, seg0 + plan.seg_len) of the readout only, with split
+// operands whatever the input type: the slices' partial readouts, summed into
+// slice 0 of partial ([slice][BH][seg_len][d_v+1]), and S_state carried
+// (from zero when first).
+hipError_t launch_prefill_feat_readout(const void* q, const void* k, const void* v, bool bf16_in, int BH, int n,
+                                       int dk, int dv, const DevTable& t, const FeatPrefillPlan& plan,
+                                       float* S_state, float* partial, int seg0, bool first, hipStream_t s);
+
 // ---- backward ----------------------------------------------------------------
 constexpr int kMaxBackwardDim = 64;
 struct BackwardPlan {
@@ -113,10 +145,12 @@ struct BackwardPlan {
   size_t partial_bytes = 0;  // partial sums of one segment
   size_t h_bytes = 0;        // dL/do for every token, float32 [BH][n][d_v+1]
   size_t state_bytes = 0;    // one float32 state [BH][D][d_v+1]
+  bool feat_fwd = false;     // the forward readout of pass 1 on the matrix cores (split operands)
+  FeatPrefillPlan feat;      // its plan (seg_len = the backward's)
 };
 // False if d_k or d_v exceeds kMaxBackwardDim, the chunk is not 16, 32 or 64,
 // or no slice fits on chip.  Also fills the forward plan of the first pass.
-bool plan_backward(int64_t D, int BH, int n, int dk, int dv, int chunk, size_t max_ws_bytes, BackwardPlan* plan,
+bool plan_backward(int64_t D, int BH, int n, int dk, int dv, int P, int chunk, size_t max_ws_bytes, BackwardPlan* plan,
                    PrefillGenericPlan* fwd);
 hipError_t launch_backward(const void* q, const void* k, const void* v, const void* dy, void* dq, void* dk,
                            void* dv, bool bf16, int BH, int n, int dk_, int dv_, int P, int chunk, const DevTable& t,

@@ -43,7 +43,6 @@
 
 #include "device_common.hpp"
 #include "kernels.hpp"
-#include "prefill_feat.hpp"
 
 namespace sata {
 
@@ -117,8 +116,9 @@ struct FeatLds {
   static constexpr int kBytes = kAll > kRedTile ? kAll : kRedTile;
 };
 
-// FT tiles of 16 features per wave, NCT column tiles; X3: float32 inputs, split operands.
-template <int NCT, int FT, bool X3>
+// FT tiles of 16 features per wave, NCT column tiles; X3: split operands;
+// T: the input element type (bf16 bits or float).
+template <int NCT, int FT, bool X3, typename T>
 __global__ void __launch_bounds__(kNW * 64, 1)
 prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, const void* __restrict__ v_,
                   const uint64_t* __restrict__ packed, const uint32_t* __restrict__ gen, int64_t D,
@@ -126,7 +126,6 @@ prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, cons
                   int seg_len, int first_seg, int qg) {
   static_assert(FT % 2 == 0, "feature tiles come in blocks of two");
   static_assert(kNW * FT * 16 <= kTablePad, "a slice may end past the last feature by less than the table's padding");
-  using T = std::conditional_t<X3, float, u16>;
   using L = FeatLds<NCT, X3>;
   constexpr int kEV = 16 / sizeof(T);  // elements per 16-byte vector
   constexpr int kVPlane = NCT * 16 * kVS;  // bf16 per V^T plane
@@ -198,24 +197,25 @@ prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, cons
     }
   };
   // element j of a 16-byte vector (j a constant after unrolling)
+  constexpr bool kF32In = std::is_same_v<T, float>;
   auto elem = [](const uint4& w, int j) -> T {
     const uint32_t u[4] = {w.x, w.y, w.z, w.w};
-    if constexpr (X3) return __uint_as_float(u[j]);
+    if constexpr (kF32In) return __uint_as_float(u[j]);
     else return (u16)(j & 1 ? u[j >> 1] >> 16 : u[j >> 1] & 0xffffu);
   };
-  auto elem_f32 = [&](const uint4& w, int j) -> float {
-    if constexpr (X3) return elem(w, j);
-    else return __uint_as_float((uint32_t)elem(w, j) << 16);
-  };
   auto to_f32 = [](T x) -> float {
-    if constexpr (X3) return x;
+    if constexpr (kF32In) return x;
     else return __uint_as_float((uint32_t)x << 16);
   };
+  auto elem_f32 = [&](const uint4& w, int j) -> float { return to_f32(elem(w, j)); };
   // V^T entry (column c, token t) of value x: both planes with split operands
   auto put_v = [&](int c, int t, T x) {
     if constexpr (X3) {
+      const float f = to_f32(x);
+      vt[c * kVS + t] = bf16_bits(f);
+      vt[kVPlane + c * kVS + t] = bf16_bits(bf16_rest(f));
+    } else if constexpr (kF32In) {
       vt[c * kVS + t] = bf16_bits(x);
-      vt[kVPlane + c * kVS + t] = bf16_bits(bf16_rest(x));
     } else {
       vt[c * kVS + t] = x;
     }
@@ -344,9 +344,9 @@ prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, cons
               }
             }
             if (W != 1) {
-              // Phi_Q: feature 8 g + r = 16 T + 4 hh + r' sits in K slot 8 hh + 4 T + r'
-              const int T = g >> 1, hh = 2 * (g & 1);
-              u16* const row = phq + lane * kQS + 4 * T;
+              // Phi_Q: feature 8 g + r = 16 tt + 4 hh + r' sits in K slot 8 hh + 4 tt + r'
+              const int tt = g >> 1, hh = 2 * (g & 1);
+              u16* const row = phq + lane * kQS + 4 * tt;
               *(uint2*)(row + 8 * hh) = uint2{pack2(vq[0], vq[1]), pack2(vq[2], vq[3])};
               *(uint2*)(row + 8 * (hh + 1)) = uint2{pack2(vq[4], vq[5]), pack2(vq[6], vq[7])};
               if (X3) {
@@ -520,13 +520,13 @@ constexpr int lds_for(int nct, bool x3) {
   }
 }
 
-template <int NCT, bool X3, int FT>
+template <int NCT, bool X3, int FT, typename T>
 hipError_t launch_main(const void* q, const void* k, const void* v, const DevTable& t, float* S_state, float* part,
                        int BH, int n, int dk, int dv, int seg0, int seg_len, bool first, int nslices, int qg,
                        hipStream_t s) {
   constexpr int bytes = FeatLds<NCT, X3>::kBytes;
   static_assert(bytes <= 160 * 1024, "LDS of one workgroup");
-  auto kern = prefill_feat_main<NCT, FT, X3>;
+  auto kern = prefill_feat_main<NCT, FT, X3, T>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3((unsigned)nslices, (unsigned)BH), dim3(kNW * 64), (size_t)bytes, s, q, k, v,
@@ -534,28 +534,38 @@ hipError_t launch_main(const void* q, const void* k, const void* v, const DevTab
   return hipGetLastError();
 }
 
-template <int NCT, bool X3>
+template <int NCT, bool X3, typename T>
 hipError_t launch_main_ft(bool narrow, const void* q, const void* k, const void* v, const DevTable& t,
                           float* S_state, float* part, int BH, int n, int dk, int dv, int seg0, int seg_len,
                           bool first, int nslices, int qg, hipStream_t s) {
   if (narrow)
-    return launch_main<NCT, X3, kNarrowFT>(q, k, v, t, S_state, part, BH, n, dk, dv, seg0, seg_len, first, nslices,
-                                           qg, s);
-  return launch_main<NCT, X3, ft_for(NCT, X3)>(q, k, v, t, S_state, part, BH, n, dk, dv, seg0, seg_len, first,
-                                               nslices, qg, s);
+    return launch_main<NCT, X3, kNarrowFT, T>(q, k, v, t, S_state, part, BH, n, dk, dv, seg0, seg_len, first,
+                                              nslices, qg, s);
+  return launch_main<NCT, X3, ft_for(NCT, X3), T>(q, k, v, t, S_state, part, BH, n, dk, dv, seg0, seg_len, first,
+                                                  nslices, qg, s);
 }
 
-template <bool X3>
+template <bool X3, typename T>
 hipError_t launch_main_nct(const FeatPrefillPlan& p, const void* q, const void* k, const void* v, const DevTable& t,
                            float* S_state, float* part, int BH, int n, int dk, int dv, int seg0, bool first, int qg,
                            hipStream_t s) {
   switch (p.nct) {
-    case 1: return launch_main_ft<1, X3>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
-    case 2: return launch_main_ft<2, X3>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
-    case 3: return launch_main_ft<3, X3>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
-    case 4: return launch_main_ft<4, X3>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
-    default: return launch_main_ft<5, X3>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
+    case 1: return launch_main_ft<1, X3, T>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
+    case 2: return launch_main_ft<2, X3, T>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
+    case 3: return launch_main_ft<3, X3, T>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
+    case 4: return launch_main_ft<4, X3, T>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
+    default: return launch_main_ft<5, X3, T>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
   }
+}
+
+// The slices' partial readouts of one segment, summed into slice 0.
+hipError_t fold_slices(float* partial, const FeatPrefillPlan& plan, int BH, int n, int dv, int seg0, hipStream_t s) {
+  if (plan.nslices <= 1) return hipSuccess;
+  const int seg_tokens = std::min(plan.seg_len, n - seg0);
+  const int64_t count = (int64_t)BH * seg_tokens * (dv + 1);
+  hipLaunchKernelGGL(reduce_slices, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, partial, BH, plan.seg_len,
+                     seg_tokens, dv + 1, plan.nslices);
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -596,25 +606,30 @@ hipError_t launch_prefill_feat(const void* q, const void* k, const void* v, void
                                hipStream_t s, int qg) {
   for (int seg0 = 0; seg0 < n; seg0 += plan.seg_len) {
     const bool first = seg0 == 0;
-    hipError_t e = plan.split ? launch_main_nct<true>(plan, q, k, v, t, S_state, partial, BH, n, dk, dv, seg0, first,
+    // float32 inputs take split operands, bf16 inputs bf16 operands
+    hipError_t e = plan.split
+                       ? launch_main_nct<true, float>(plan, q, k, v, t, S_state, partial, BH, n, dk, dv, seg0, first,
                                                       qg, s)
-                              : launch_main_nct<false>(plan, q, k, v, t, S_state, partial, BH, n, dk, dv, seg0, first,
-                                                       qg, s);
+                       : launch_main_nct<false, u16>(plan, q, k, v, t, S_state, partial, BH, n, dk, dv, seg0, first,
+                                                     qg, s);
     if (e != hipSuccess) return e;
-    int ns = plan.nslices;
-    if (ns > 1) {
-      const int seg_tokens = std::min(plan.seg_len, n - seg0);
-      const int64_t count = (int64_t)BH * seg_tokens * (dv + 1);
-      hipLaunchKernelGGL(reduce_slices, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, partial, BH,
-                         plan.seg_len, seg_tokens, dv + 1, ns);
-      if ((e = hipGetLastError()) != hipSuccess) return e;
-      ns = 1;
-    }
-    e = launch_prefill_generic_finalize(q, k, v, y, !plan.split, BH, n, dk, dv, P, kCh, ns, seg0, plan.seg_len,
-                                        partial, s, qg);
+    if ((e = fold_slices(partial, plan, BH, n, dv, seg0, s)) != hipSuccess) return e;
+    e = launch_prefill_generic_finalize(q, k, v, y, !plan.split, BH, n, dk, dv, P, kCh, 1, seg0, plan.seg_len, partial,
+                                        s, qg);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+hipError_t launch_prefill_feat_readout(const void* q, const void* k, const void* v, bool bf16_in, int BH, int n,
+                                       int dk, int dv, const DevTable& t, const FeatPrefillPlan& plan,
+                                       float* S_state, float* partial, int seg0, bool first, hipStream_t s) {
+  hipError_t e = bf16_in ? launch_main_nct<true, u16>(plan, q, k, v, t, S_state, partial, BH, n, dk, dv, seg0, first,
+                                                      1, s)
+                         : launch_main_nct<true, float>(plan, q, k, v, t, S_state, partial, BH, n, dk, dv, seg0,
+                                                        first, 1, s);
+  if (e != hipSuccess) return e;
+  return fold_slices(partial, plan, BH, n, dv, seg0, s);
 }
 
 }  // namespace sata

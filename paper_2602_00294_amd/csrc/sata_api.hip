@@ -13,7 +13,6 @@
 
 #include "kernels.hpp"
 #include "prefill_blocks.hpp"
-#include "prefill_feat.hpp"
 #include "prefill_mfma.hpp"
 #include "sata.h"
 #include "table.hpp"
@@ -514,7 +513,7 @@ sata_status sata_backward(const void* q, const void* k, const void* v, const voi
   const int BH = B * H;
   sata::BackwardPlan plan;
   sata::PrefillGenericPlan fwd;
-  if (!sata::plan_backward(D, BH, n, d_k, d_v, chunk, kMaxWorkspace, &plan, &fwd))
+  if (!sata::plan_backward(D, BH, n, d_k, d_v, P, chunk, kMaxWorkspace, &plan, &fwd))
     return fail(SATA_ERR_UNSUPPORTED, "no backward slice fits on chip for d_k=%d d_v=%d chunk=%d", d_k, d_v, chunk);
   hipStream_t s = (hipStream_t)stream;
   sata::DevTable t;

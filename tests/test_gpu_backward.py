@@ -44,6 +44,8 @@ def _rel(a, b):
     (1, 1, 200, 32, 32, 4, 64, "bf16"),   # the benchmark's head shape
     (1, 1, 45, 5, 3, 1, 16, "f32"),       # P = 1: no gradient for q and k
     (1, 1, 300, 8, 8, 2, 64, "f32"),
+    (1, 1, 150, 4, 4, 6, 64, "f32"),      # degrees above 3 (the full product rule)
+    (1, 1, 100, 64, 64, 3, 64, "bf16"),   # the largest head, five column tiles in the forward readout
 ])
 def test_backward_matches_oracle(sata, B, H, n, dk, dv, P, chunk, dtype):
     _say(f"backward B={B} H={H} n={n} dk={dk} dv={dv} P={P} chunk={chunk} {dtype}")
