@@ -99,7 +99,8 @@ sata_status sata_feature_map(const void* x, sata_dtype xt, int64_t rows, int d, 
  * {16, 32}) keep every token's float32 partial readouts (576 bytes per head
  * and token at d_k = 32, chunk 64) and serve a call only while those fit in
  * 4 GB; longer calls, and every other shape, work in segments whose partial
- * sums take at most 512 MB, so the workspace stays bounded for any n.
+ * sums take at most 2 GB (512 MB on the float32 vector path), so the
+ * workspace stays bounded for any n.
  * SATA_ERR_HIP if the workspace cannot be allocated; SATA_ERR_UNSUPPORTED if
  * a chunk's tiles do not fit on chip (for example d_k = 255 with chunk 64). */
 sata_status sata_prefill(const void* q, const void* k, const void* v, sata_dtype dt,
@@ -138,7 +139,7 @@ sata_status sata_prefill_grouped(const void* q, const void* k, const void* v, sa
  * All arithmetic is float32 (the forward is recomputed, not passed in).
  * chunk: 16, 32 or 64; d_k, d_v <= 64 (SATA_ERR_UNSUPPORTED otherwise).
  * Workspace: float32 dL/d[N|Z] for every token (4 (d_v+1) bytes per
- * head-token), one state, and per-segment partial sums of at most 512 MB.
+ * head-token), one state, and per-segment partial sums of at most 2 GB.
  * n = 0 writes nothing. */
 sata_status sata_backward(const void* q, const void* k, const void* v, const void* dy, sata_dtype dt,
                           int B, int H, int n, int d_k, int d_v, int P, int chunk,

@@ -72,6 +72,9 @@ constexpr size_t kMaxWorkspace = (size_t)512 << 20;
 // reload the whole state (at d = 64 a 4096-token call of 16 heads is one
 // segment).
 constexpr size_t kMaxFeatWorkspace = (size_t)2 << 30;
+// The same for the backward, whose scan workgroups load and store their state
+// slice at every segment.
+constexpr size_t kMaxBackwardWorkspace = (size_t)2 << 30;
 // The tuned matrix-core kernels hold the partial readouts of the whole call;
 // beyond this much the call takes the segmented kernels instead.
 constexpr size_t kMaxWholeCallWorkspace = (size_t)4 << 30;
@@ -513,7 +516,7 @@ sata_status sata_backward(const void* q, const void* k, const void* v, const voi
   const int BH = B * H;
   sata::BackwardPlan plan;
   sata::PrefillGenericPlan fwd;
-  if (!sata::plan_backward(D, BH, n, d_k, d_v, P, chunk, kMaxWorkspace, &plan, &fwd))
+  if (!sata::plan_backward(D, BH, n, d_k, d_v, P, chunk, kMaxBackwardWorkspace, &plan, &fwd))
     return fail(SATA_ERR_UNSUPPORTED, "no backward slice fits on chip for d_k=%d d_v=%d chunk=%d", d_k, d_v, chunk);
   hipStream_t s = (hipStream_t)stream;
   sata::DevTable t;
