@@ -55,20 +55,20 @@ struct GroupRow<8> {
   }
 };
 
-// LDS layout (floats): fk [rows4] | fq [rows4][G] | xq [G][dk] | xk [dk] |
+// LDS layout (floats): fk [rows4] | fq [rows4][G] | xq [G][dk+1] | xk [dk+1] |
 // ve [E] | red [2][4 tu] | part [2][8][E] | o [G][E] | lo_val [G][8] | lo_col [8]
 // with rows4 = max_rows rounded up to a multiple of 4 (fq 16-byte aligned).
 __host__ __device__ inline size_t grouped_lds_floats(int max_rows, int G, int dk, int E, int tu) {
   const size_t rows4 = ((size_t)max_rows + 3) & ~(size_t)3;
-  return rows4 * (1 + G) + (size_t)G * dk + dk + E + 8 * (size_t)tu + 16 * (size_t)E + (size_t)G * E + 8 * (size_t)G +
-         8;
+  return rows4 * (1 + G) + (size_t)G * (dk + 1) + (dk + 1) + E + 8 * (size_t)tu + 16 * (size_t)E + (size_t)G * E +
+         8 * (size_t)G + 8;
 }
 
 template <typename T, int NTH, int G>
 __global__ void __launch_bounds__(NTH, (G <= 2 ? 8 : 4))
 decode_grouped_kernel(float* __restrict__ S, const T* __restrict__ q, const T* __restrict__ k,
                       const T* __restrict__ v, T* __restrict__ y, const uint64_t* __restrict__ packed,
-                      const float* __restrict__ weight, int64_t D, int dk, int dv, int tu, int npieces, int steps,
+                      const uint32_t* __restrict__ gen, int64_t D, int dk, int dv, int tu, int npieces, int steps,
                       int max_rows, float* __restrict__ xpart, int* __restrict__ cnt, float even_share) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
   const int E = dv + 1;
@@ -88,8 +88,8 @@ decode_grouped_kernel(float* __restrict__ S, const T* __restrict__ q, const T* _
   float* const fk = lds;
   float* const fq = fk + rows4;
   float* const xq = fq + (size_t)rows4 * G;
-  float* const xk = xq + G * dk;
-  float* const ve = xk + dk;
+  float* const xk = xq + G * (dk + 1);
+  float* const ve = xk + dk + 1;
   float* const red = ve + E;       // [2][4 tu]
   float* const part = red + 8 * tu;  // [2][8][E]
   float* const o = part + 16 * E;
@@ -111,8 +111,13 @@ decode_grouped_kernel(float* __restrict__ S, const T* __restrict__ q, const T* _
   row_hi = min<int64_t>(row_hi, row_lo + max_rows - 1);  // never past the LDS rows (the plan bounds them)
 
   // the G query vectors of this key/value head are rows bh G .. bh G + G - 1
-  for (int i = tid; i < G * dk; i += NTH) xq[i] = to_f32(q[bh * G * dk + i]);
-  for (int i = tid; i < dk; i += NTH) xk[i] = to_f32(k[bh * dk + i]);
+  // coordinates with a column dk held at 1 (read by the generation program
+  // for degree-0 features and missing indices)
+  for (int i = tid; i < G * (dk + 1); i += NTH) {
+    const int g = i / (dk + 1), c = i - g * (dk + 1);
+    xq[i] = c < dk ? to_f32(q[(bh * G + g) * dk + c]) : 1.0f;
+  }
+  for (int i = tid; i <= dk; i += NTH) xk[i] = i < dk ? to_f32(k[bh * dk + i]) : 1.0f;
   for (int i = tid; i < E; i += NTH) ve[i] = (i < dv) ? to_f32(v[bh * dv + i]) : 1.0f;
   const bool lead = lt >= 0 && lt < nleft;
   float lx = Sh[lead ? le : 0];
@@ -123,34 +128,45 @@ decode_grouped_kernel(float* __restrict__ S, const T* __restrict__ q, const T* _
     cur[u] = Sv[(active && g < nv && m_lo + u < m_hi) ? g : 0];
   }
   lx = lead ? lx : 0.0f;
-  // the first two table entries of this thread's rows load while the
-  // coordinates reach LDS (the barrier waits for LDS only)
-  uint64_t pk0[2];
-  float w0[2];
+  // the first two generation-program entries of this thread's rows load
+  // while the coordinates reach LDS (the barrier waits for LDS only)
+  uint2 gw[2];
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int64_t f = row_lo + tid + (int64_t)NTH * u;
-    pk0[u] = (f <= row_hi) ? packed[f] : 0;
-    w0[u] = (f <= row_hi) ? weight[f] : 0.0f;
+    gw[u] = (f <= row_hi) ? ((const uint2*)gen)[f] : uint2{0u, 0u};
   }
   lds_wait_barrier();
+  // one feature at the G + 1 coordinate rows: weight times the coordinates of
+  // the last index and the first two others (the column dk where missing),
+  // times any further indices from the packed entry
+  auto features = [&](uint2 g2, int64_t f, int64_t r) {
+    const float w = __uint_as_float(g2.y);
+    const int il = (int)((g2.x & 0x3ffu) >> 2), i0 = (int)((g2.x >> 10) & 0xffu), i1 = (int)((g2.x >> 18) & 0xffu);
+    uint64_t e = 0;
+    int p = 0;
+    if ((g2.x >> 30) & 1u) {
+      e = packed[f];
+      p = (int)(e >> 56);
+    }
+    float vk = w * xk[i0] * xk[i1] * xk[il];
+    for (int j = 2; j < p - 1; ++j) vk *= xk[(e >> (8 * j)) & 0xff];
+    fk[r] = vk;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float* const xg = xq + g * (dk + 1);
+      float vq = w * xg[i0] * xg[i1] * xg[il];
+      for (int j = 2; j < p - 1; ++j) vq *= xg[(e >> (8 * j)) & 0xff];
+      fq[r * G + g] = vq;
+    }
+  };
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int64_t r = tid + (int64_t)NTH * u;
-    if (row_lo + r <= row_hi) {
-      fk[r] = feature_value(pk0[u], w0[u], xk);
-#pragma unroll
-      for (int g = 0; g < G; ++g) fq[r * G + g] = feature_value(pk0[u], w0[u], xq + g * dk);
-    }
+    if (row_lo + r <= row_hi) features(gw[u], row_lo + r, r);
   }
-  for (int64_t f = row_lo + tid + 2 * (int64_t)NTH; f <= row_hi; f += NTH) {
-    const uint64_t pk = packed[f];
-    const float w = weight[f];
-    const int64_t r = f - row_lo;
-    fk[r] = feature_value(pk, w, xk);
-#pragma unroll
-    for (int g = 0; g < G; ++g) fq[r * G + g] = feature_value(pk, w, xq + g * dk);
-  }
+  for (int64_t f = row_lo + tid + 2 * (int64_t)NTH; f <= row_hi; f += NTH)
+    features(((const uint2*)gen)[f], f, f - row_lo);
   lds_wait_barrier();
   if (lead) {
     const int64_t f = le / E;
@@ -290,9 +306,12 @@ GroupedDecodePlan plan_decode_grouped(int64_t D, int dk, int dv, int BH, int G) 
   const int tu = (nth / unit) * unit;
   if (tu <= 0 || 8 * E > nth) return p;
   const int64_t steps = (D * E / 4 + tu - 1) / tu;
+  // pieces per head: at least one 1024-thread workgroup per compute unit (256)
+  // while a piece keeps 4 steps per thread, then up to two while it keeps 8
   int np = 1;
   if (nth == 1024 && steps >= 4) {
     np = 2;
+    while ((int64_t)BH * np < 256 && steps / (2 * np) >= 4 && np < 64) np *= 2;
     while ((int64_t)BH * np < 512 && steps / (2 * np) >= 8 && np < 64) np *= 2;
   }
   // rows a piece touches at most: its steps (the larger share of a pair, plus
@@ -334,7 +353,7 @@ hipError_t launch_decode_grouped(float* S, const void* q, const void* k, const v
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)plan.lds);                      \
     if (e != hipSuccess) return e;                                                                            \
     hipLaunchKernelGGL((decode_grouped_kernel<TT, NTH, GG>), dim3((unsigned)BH * (unsigned)plan.np), dim3(NTH), \
-                       plan.lds, s, S, (const TT*)q, (const TT*)k, (const TT*)v, (TT*)y, t.packed, t.weight, t.D,   \
+                       plan.lds, s, S, (const TT*)q, (const TT*)k, (const TT*)v, (TT*)y, t.packed, t.gen, t.D,   \
                        dk, dv, plan.tu, plan.np, plan.steps, plan.rows, partial, counters, plan.even_share);  \
   } while (0)
 #define SATA_DECODE_GROUPED_G(TT, NTH)                  \
