@@ -516,14 +516,16 @@ __global__ void decode_finalize_kernel(const float* __restrict__ partial, T* __r
 template <typename T>
 __device__ void load_chunk(const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
                            int64_t bh, int n, int t0, int cn, int C, int dk, int dv, float* xq, float* xk,
-                           float* ve, int qg) {
+                           float* ve, int qg, int XS) {
+  // xq, xk: [C][XS] (XS >= dk); ve: [C][d_v + 1] with the constant-1 column
   const int E = dv + 1;
   const int64_t qoff = (bh * qg * n + t0) * (int64_t)dk;
   const int64_t koff = (bh * n + t0) * (int64_t)dk;
   for (int i = threadIdx.x; i < C * dk; i += kThreads) {
     const int t = i / dk;
-    xq[i] = t < cn ? to_f32(q[qoff + i]) : 0.0f;
-    xk[i] = t < cn ? to_f32(k[koff + i]) : 0.0f;
+    const int c = i - t * dk;
+    xq[t * XS + c] = t < cn ? to_f32(q[qoff + i]) : 0.0f;
+    xk[t * XS + c] = t < cn ? to_f32(k[koff + i]) : 0.0f;
   }
   const int64_t voff = (bh * n + t0) * (int64_t)dv;
   for (int i = threadIdx.x; i < C * E; i += kThreads) {
@@ -569,7 +571,7 @@ prefill_generic_main(const T* __restrict__ q, const T* __restrict__ k, const T* 
   for (int t0 = seg0; t0 < seg_end; t0 += C) {
     const int cn = min(C, n - t0);
     __syncthreads();
-    load_chunk(q, k, v, bh, n, t0, cn, C, dk, dv, xq, xk, ve, qg);
+    load_chunk(q, k, v, bh, n, t0, cn, C, dk, dv, xq, xk, ve, qg, dk);
     __syncthreads();
     for (int i = tid; i < cn * fs; i += kThreads) {
       const int t = i / fs;
@@ -636,6 +638,7 @@ prefill_generic_main(const T* __restrict__ q, const T* __restrict__ k, const T* 
 }
 
 constexpr int kFinRows = 32;
+__host__ __device__ constexpr int fin_stride(int dk) { return dk | 1; }
 
 template <typename T>
 __global__ void __launch_bounds__(kThreads)
@@ -644,9 +647,11 @@ prefill_generic_finalize(const T* __restrict__ q, const T* __restrict__ k, const
                          int P, int C, int nslices, int seg0, int seg_len, int qg) {
   extern __shared__ float lds[];
   const int E = dv + 1;
-  float* xq = lds;                 // [C][dk]
-  float* xk = xq + C * dk;         // [C][dk]
-  float* ve = xk + C * dk;         // [C][E]
+  // odd row stride: the lanes of the QK^T loop read different key rows
+  const int XS = fin_stride(dk);
+  float* xq = lds;                 // [C][XS]
+  float* xk = xq + C * XS;         // [C][XS]
+  float* ve = xk + C * XS;         // [C][E]
   float* A = ve + C * E;           // [kFinRows][C]
   float* O = A + kFinRows * C;     // [kFinRows][E]
   const int64_t bh = blockIdx.y;
@@ -655,7 +660,7 @@ prefill_generic_finalize(const T* __restrict__ q, const T* __restrict__ k, const
   const int cn = min(C, n - t0);
   const int tid = threadIdx.x;
   const float scale = 1.0f / sqrtf((float)dk);
-  load_chunk(q, k, v, bh, n, t0, cn, C, dk, dv, xq, xk, ve, qg);
+  load_chunk(q, k, v, bh, n, t0, cn, C, dk, dv, xq, xk, ve, qg, XS);
   __syncthreads();
   for (int rb = 0; rb < cn; rb += kFinRows) {
     const int rn = min(kFinRows, cn - rb);
@@ -666,7 +671,7 @@ prefill_generic_finalize(const T* __restrict__ q, const T* __restrict__ k, const
       float a = 0.0f;
       if (tp <= t) {
         float dot = 0.0f;
-        for (int c = 0; c < dk; ++c) dot += xq[t * dk + c] * xk[tp * dk + c];
+        for (int c = 0; c < dk; ++c) dot += xq[t * XS + c] * xk[tp * XS + c];
         a = taylor_horner(dot * scale, P);
       }
       A[i] = a;
@@ -888,7 +893,7 @@ bool plan_prefill_generic(int64_t D, int BH, int n, int dk, int dv, int chunk, s
   plan->fs = (int)fs;
   plan->nslices = (int)((D + fs - 1) / fs);
   plan->lds_main = fixed + per_feature * (size_t)fs;
-  plan->lds_final = sizeof(float) * ((size_t)2 * C * dk + (size_t)C * E + (size_t)kFinRows * C +
+  plan->lds_final = sizeof(float) * ((size_t)2 * C * fin_stride(dk) + (size_t)C * E + (size_t)kFinRows * C +
                                      (size_t)kFinRows * E);
   if (plan->lds_main > kLdsBudget || plan->lds_final > kLdsBudget) return false;
   // partial readouts for one segment: [nslices][BH][seg_len][E]
@@ -981,7 +986,8 @@ hipError_t launch_prefill_generic_finalize(const void* q, const void* k, const v
                                            int seg_len, const float* partial, hipStream_t s, int qg) {
   const int C = chunk;
   const int E = dv + 1;
-  const size_t lds = sizeof(float) * ((size_t)2 * C * dk + (size_t)C * E + (size_t)kFinRows * C + (size_t)kFinRows * E);
+  const size_t lds =
+      sizeof(float) * ((size_t)2 * C * fin_stride(dk) + (size_t)C * E + (size_t)kFinRows * C + (size_t)kFinRows * E);
   const int seg_tokens = std::min(seg_len, n - seg0);
   dim3 g2((unsigned)((seg_tokens + C - 1) / C), (unsigned)BH);
   hipError_t e;
