@@ -165,6 +165,17 @@ typedef enum {
 sata_status sata_prefill_operands(sata_dtype dt, int B, int H, int n, int d_k, int d_v, int P, int chunk,
                                   sata_operands* operands);
 
+/* Number of parts of the sequence that sata_prefill runs side by side for
+ * these arguments (host only, no GPU use; same validation as sata_prefill).
+ * 1: the chunked scan of App. A2 runs token after token.  k > 1 (a call with
+ * few heads and few features on the matrix-core path, whose sequence fits one
+ * segment): a first pass forms each part's state increment, sum over its
+ * tokens of phi(k) (x) [v, 1], and the scan of part g then starts from the sum
+ * of the increments of parts 0..g-1, the same state up to the order of the
+ * float32 additions; the workspace grows by (k - 1) states. */
+sata_status sata_prefill_parts(sata_dtype dt, int B, int H, int n, int d_k, int d_v, int P, int chunk,
+                               int* parts);
+
 /* One decode step for every (b, h) (App. A2, the linear recurrences for Z_{p,T}
  * and S_{p,T}, then the readout at q_T): S += phi(k) (x) [v, 1], then
  * y = (phi(q)^T S)[0:d_v] / (phi(q)^T S)[d_v].  The update comes first, so the

@@ -8,7 +8,7 @@ libsata.so); this package is the thin Python binding over it.
     y_t = decode_step(S, q_t, k_t, v_t, P=4)     # S updated in place
 """
 from ._binding import (SataError, backward, decode_step, decode_step_compensated, decode_step_grouped, feature_count, feature_index, feature_map, load_library,
-                       prefill, prefill_grouped, prefill_operands, release, residual_elems, state_elems)
+                       prefill, prefill_grouped, prefill_operands, prefill_parts, release, residual_elems, state_elems)
 
 __all__ = ["SataError", "backward", "decode_step", "decode_step_compensated", "decode_step_grouped", "feature_count", "feature_index", "feature_map", "load_library",
-           "prefill", "prefill_grouped", "prefill_operands", "release", "residual_elems", "state_elems"]
+           "prefill", "prefill_grouped", "prefill_operands", "prefill_parts", "release", "residual_elems", "state_elems"]

@@ -54,6 +54,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.sata_backward.restype = i32
     lib.sata_prefill_operands.argtypes = [i32, i32, i32, i32, i32, i32, i32, i32, ctypes.POINTER(i32)]
     lib.sata_prefill_operands.restype = i32
+    lib.sata_prefill_parts.argtypes = [i32, i32, i32, i32, i32, i32, i32, i32, ctypes.POINTER(i32)]
+    lib.sata_prefill_parts.restype = i32
     lib.sata_decode_step.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp]
     lib.sata_decode_step.restype = i32
     lib.sata_decode_step_noalloc.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp]
@@ -188,6 +190,19 @@ def prefill_operands(dtype, B: int, H: int, n: int, d_k: int, d_v: int, P: int, 
     _check(load_library().sata_prefill_operands(code, B, H, n, d_k, d_v, P, chunk, ctypes.byref(out)),
            "sata_prefill_operands")
     return {0: "f32", 1: "bf16", 2: "split"}[out.value]
+
+
+def prefill_parts(dtype, B: int, H: int, n: int, d_k: int, d_v: int, P: int, chunk: int = 64) -> int:
+    """Number of parts of the sequence that prefill runs side by side for these
+    arguments (host only; 1: one scan from the first token to the last)."""
+    torch = _torch()
+    code = {torch.float32: SATA_F32, torch.bfloat16: SATA_BF16}.get(dtype)
+    if code is None:
+        raise TypeError(f"unsupported dtype {dtype}; use float32 or bfloat16")
+    out = ctypes.c_int(-1)
+    _check(load_library().sata_prefill_parts(code, B, H, n, d_k, d_v, P, chunk, ctypes.byref(out)),
+           "sata_prefill_parts")
+    return out.value
 
 
 def prefill(q, k, v, P: int, chunk: int = 64, want_state: bool = True, y=None, S=None):

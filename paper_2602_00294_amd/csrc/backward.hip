@@ -598,6 +598,8 @@ bool plan_backward(int64_t D, int BH, int n, int dk, int dv, int P, int chunk, s
   plan->partial_bytes = per_token * (size_t)plan->seg_len;
   fwd->seg_len = plan->seg_len;
   plan->feat.seg_len = plan->seg_len;
+  plan->feat.parts = 1;  // (the backward's forward readout runs its segments in order)
+  plan->feat.part_len = plan->seg_len;
   plan->h_bytes = sizeof(float) * (size_t)BH * n * E;
   plan->state_bytes = sizeof(float) * (size_t)BH * D * E;
   return true;

@@ -111,8 +111,11 @@ struct FeatPrefillPlan {
   bool narrow = false;     // slices of 256 features (for few features or few heads)
   int nslices = 0;         // workgroups per head
   int seg_len = 0;         // tokens per segment (partial sums of one segment in the workspace)
+  int parts = 1;           // parts of a one-segment call that run side by side (states summed first)
+  int part_len = 0;        // tokens per part
+  size_t part_state_offset = 0;  // workspace bytes before the parts' states
   size_t lds_main = 0;
-  size_t partial_bytes = 0;
+  size_t partial_bytes = 0;  // the whole workspace: partials, then the parts' states
 };
 
 // True if the kernel covers this shape (chunk 64, P >= 2, d_k, d_v <= 64).

@@ -116,14 +116,27 @@ struct FeatLds {
   static constexpr int kBytes = kAll > kRedTile ? kAll : kRedTile;
 };
 
+// Where the parts of a launch (blockIdx.z) start and leave their states, each
+// [BH][D][d_v+1] float32.  Part 0 starts from in0, part g >= 1 from
+// in + (g - 1) * stride (null: from zero); the last part stores to last, the
+// others (and the last, when last is null) to out + g * stride (null: not
+// stored).
+struct FeatStates {
+  const float* in0;
+  const float* in;
+  float* last;
+  float* out;
+};
+
 // FT tiles of 16 features per wave, NCT column tiles; X3: split operands;
-// T: the input element type (bf16 bits or float).
-template <int NCT, int FT, bool X3, typename T>
+// T: the input element type (bf16 bits or float); RO: with the readout (else
+// the parts' state sums alone).
+template <int NCT, int FT, bool X3, typename T, bool RO>
 __global__ void __launch_bounds__(kNW * 64, 1)
 prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, const void* __restrict__ v_,
                   const uint64_t* __restrict__ packed, const uint32_t* __restrict__ gen, int64_t D,
-                  float* __restrict__ S_state, float* __restrict__ part, int BH, int n, int dk, int dv, int seg0,
-                  int seg_len, int first_seg, int qg) {
+                  FeatStates st, float* __restrict__ part, int BH, int n, int dk, int dv, int seg0, int seg_len,
+                  int part_len, int qg) {
   static_assert(FT % 2 == 0, "feature tiles come in blocks of two");
   static_assert(kNW * FT * 16 <= kTablePad, "a slice may end past the last feature by less than the table's padding");
   using L = FeatLds<NCT, X3>;
@@ -151,6 +164,12 @@ prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, cons
   const int fslice = slice * kNW * FT * 16;  // (features fit 32 bits: D <= 2^26)
   const int Di = (int)D;
   const int fw0 = fslice + wave * FT * 16;  // this wave's first feature
+  // part blockIdx.z of the segment: its tokens, and where its state starts and ends
+  const int pz = blockIdx.z;
+  const int64_t sstride = (int64_t)BH * D * E;
+  const float* const s_in = pz == 0 ? st.in0 : (st.in ? st.in + (pz - 1) * sstride : nullptr);
+  float* const s_out = (pz == (int)gridDim.z - 1 && st.last) ? st.last : (st.out ? st.out + pz * sstride : nullptr);
+  const int t_begin = seg0 + pz * part_len;
 
   // the state tiles: S[t][j] holds features fw0 + 16 t + 4 h4 + r, column 16 j + l15
   f32x4 S[FT][NCT];
@@ -159,12 +178,12 @@ prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, cons
 #pragma unroll
     for (int j = 0; j < NCT; ++j) {
       f32x4 s = {0.f, 0.f, 0.f, 0.f};
-      if (!first_seg) {
+      if (s_in) {
         const int c = 16 * j + l15;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int f = fw0 + 16 * t + 4 * h4 + r;
-          if (f < Di && c < E) s[r] = S_state[(bh * D + f) * E + c];
+          if (f < Di && c < E) s[r] = s_in[(bh * D + f) * E + c];
         }
       }
       S[t][j] = s;
@@ -173,7 +192,7 @@ prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, cons
   const T* const qh = (const T*)q_ + bh * (int64_t)qg * n * dk;
   const T* const kh = (const T*)k_ + bh * (int64_t)n * dk;
   const T* const vh = (const T*)v_ + bh * (int64_t)n * dv;
-  const int seg_end = min(n, seg0 + seg_len);
+  const int seg_end = min(min(n, seg0 + seg_len), t_begin + part_len);
   // The next chunk's q, k and v are fetched into registers (16-byte vectors of
   // one row) while the current chunk is processed, when every row of the head
   // starts 16-byte aligned; otherwise element by element.
@@ -220,8 +239,8 @@ prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, cons
       vt[c * kVS + t] = x;
     }
   };
-  if (vec) fetch(seg0);
-  for (int t0 = seg0; t0 < seg_end; t0 += kCh) {
+  if (vec) fetch(t_begin);
+  for (int t0 = t_begin; t0 < seg_end; t0 += kCh) {
     const int cn = min(kCh, n - t0);
     __syncthreads();  // the previous chunk's reduction has read its buffer
     if (vec) {
@@ -424,7 +443,11 @@ prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, cons
           }
         };
         lds_fence();  // the previous block's operand reads have completed
-        if constexpr (X3) {
+        if constexpr (!RO) {  // the state sum alone
+          generate(std::integral_constant<int, 1>{});
+          lds_fence();
+          update();
+        } else if constexpr (X3) {
           generate(std::integral_constant<int, 0>{});
           lds_fence();
           readout();
@@ -441,6 +464,7 @@ prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, cons
       }
     });
 
+    if constexpr (!RO) continue;
     // ---- the waves' partial readouts, added in wave order, TP token tiles at
     // a time; a lane's four rows of a column are one 16-byte store
     float* const pout = part + (((int64_t)slice * BH + bh) * seg_len + (t0 - seg0)) * E;
@@ -479,7 +503,7 @@ prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, cons
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int f = fw0 + 16 * t + 4 * h4 + r;
-        if (f < Di && c < E) S_state[(bh * D + f) * E + c] = S[t][j][r];
+        if (f < Di && c < E && s_out) s_out[(bh * D + f) * E + c] = S[t][j][r];
       }
     }
 }
@@ -529,41 +553,56 @@ constexpr int lds_for(int nct, bool x3) {
   }
 }
 
+// One launch over the parts of a segment: `parts` workgroups per (slice,
+// head), each taking part_len tokens.
+struct FeatLaunch {
+  FeatStates st;
+  int seg0, seg_len, part_len, parts;
+  bool readout;
+};
+
 template <int NCT, bool X3, int FT, typename T>
-hipError_t launch_main(const void* q, const void* k, const void* v, const DevTable& t, float* S_state, float* part,
-                       int BH, int n, int dk, int dv, int seg0, int seg_len, bool first, int nslices, int qg,
-                       hipStream_t s) {
+hipError_t launch_main(const void* q, const void* k, const void* v, const DevTable& t, const FeatLaunch& fl,
+                       float* part, int BH, int n, int dk, int dv, int nslices, int qg, hipStream_t s) {
   constexpr int bytes = FeatLds<NCT, X3>::kBytes;
   static_assert(bytes <= 160 * 1024, "LDS of one workgroup");
-  auto kern = prefill_feat_main<NCT, FT, X3, T>;
+  auto kern = fl.readout ? prefill_feat_main<NCT, FT, X3, T, true> : prefill_feat_main<NCT, FT, X3, T, false>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3((unsigned)nslices, (unsigned)BH), dim3(kNW * 64), (size_t)bytes, s, q, k, v,
-                     t.packed, t.gen, t.D, S_state, part, BH, n, dk, dv, seg0, seg_len, first ? 1 : 0, qg);
+  hipLaunchKernelGGL(kern, dim3((unsigned)nslices, (unsigned)BH, (unsigned)fl.parts), dim3(kNW * 64), (size_t)bytes, s,
+                     q, k, v, t.packed, t.gen, t.D, fl.st, part, BH, n, dk, dv, fl.seg0, fl.seg_len, fl.part_len, qg);
   return hipGetLastError();
 }
 
 template <int NCT, bool X3, typename T>
 hipError_t launch_main_ft(bool narrow, const void* q, const void* k, const void* v, const DevTable& t,
-                          float* S_state, float* part, int BH, int n, int dk, int dv, int seg0, int seg_len,
-                          bool first, int nslices, int qg, hipStream_t s) {
-  if (narrow)
-    return launch_main<NCT, X3, kNarrowFT, T>(q, k, v, t, S_state, part, BH, n, dk, dv, seg0, seg_len, first,
-                                              nslices, qg, s);
-  return launch_main<NCT, X3, ft_for(NCT, X3), T>(q, k, v, t, S_state, part, BH, n, dk, dv, seg0, seg_len, first,
-                                                  nslices, qg, s);
+                          const FeatLaunch& fl, float* part, int BH, int n, int dk, int dv, int nslices, int qg,
+                          hipStream_t s) {
+  if (narrow) return launch_main<NCT, X3, kNarrowFT, T>(q, k, v, t, fl, part, BH, n, dk, dv, nslices, qg, s);
+  return launch_main<NCT, X3, ft_for(NCT, X3), T>(q, k, v, t, fl, part, BH, n, dk, dv, nslices, qg, s);
 }
 
 template <bool X3, typename T>
 hipError_t launch_main_nct(const FeatPrefillPlan& p, const void* q, const void* k, const void* v, const DevTable& t,
-                           float* S_state, float* part, int BH, int n, int dk, int dv, int seg0, bool first, int qg,
-                           hipStream_t s) {
+                           const FeatLaunch& fl, float* part, int BH, int n, int dk, int dv, int qg, hipStream_t s) {
   switch (p.nct) {
-    case 1: return launch_main_ft<1, X3, T>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
-    case 2: return launch_main_ft<2, X3, T>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
-    case 3: return launch_main_ft<3, X3, T>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
-    case 4: return launch_main_ft<4, X3, T>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
-    default: return launch_main_ft<5, X3, T>(p.narrow, q, k, v, t, S_state, part, BH, n, dk, dv, seg0, p.seg_len, first, p.nslices, qg, s);
+    case 1: return launch_main_ft<1, X3, T>(p.narrow, q, k, v, t, fl, part, BH, n, dk, dv, p.nslices, qg, s);
+    case 2: return launch_main_ft<2, X3, T>(p.narrow, q, k, v, t, fl, part, BH, n, dk, dv, p.nslices, qg, s);
+    case 3: return launch_main_ft<3, X3, T>(p.narrow, q, k, v, t, fl, part, BH, n, dk, dv, p.nslices, qg, s);
+    case 4: return launch_main_ft<4, X3, T>(p.narrow, q, k, v, t, fl, part, BH, n, dk, dv, p.nslices, qg, s);
+    default: return launch_main_ft<5, X3, T>(p.narrow, q, k, v, t, fl, part, BH, n, dk, dv, p.nslices, qg, s);
+  }
+}
+
+// Sp[g] += Sp[g - 1] for g = 1 .. parts - 2, in order: part g + 1 of the
+// readout pass starts from Sp[g], the sum of the state increments of parts 0..g.
+__global__ void __launch_bounds__(256) prefix_part_states(float* __restrict__ Sp, int64_t count, int parts) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= count) return;
+  float a = Sp[i];
+  for (int g = 1; g + 1 < parts; ++g) {
+    a += Sp[g * count + i];
+    Sp[g * count + i] = a;
   }
 }
 
@@ -607,20 +646,58 @@ bool plan_prefill_feat(int64_t D, int BH, int n, int dk, int dv, int P, int chun
   const int64_t n_round = ((int64_t)n + kCh - 1) / kCh * kCh;
   plan->seg_len = (int)std::min<int64_t>(seg, n_round);
   plan->partial_bytes = per_token * (size_t)plan->seg_len;
+  // Few workgroups (few heads with few features): a call that fits one
+  // segment is cut into parts of at least 1024 tokens that run side by side,
+  // up to one workgroup per compute unit.  A first pass sums each part's state
+  // increment, and the readout pass starts part g from the sum of the
+  // increments of parts 0 .. g-1 (kept after the partials in the workspace).
+  plan->parts = 1;
+  plan->part_len = plan->seg_len;
+  plan->part_state_offset = 0;
+  const int64_t wgs = (int64_t)plan->nslices * BH;
+  if (plan->seg_len >= n_round) {
+    int parts = 1;
+    while (parts < 16 && wgs * parts * 2 <= 256 && n_round / (2 * parts) >= 1024) parts *= 2;
+    if (parts > 1) {
+      const int64_t plen = (n_round / parts + kCh - 1) / kCh * kCh;
+      const size_t off = (plan->partial_bytes + 255) / 256 * 256;
+      const size_t sbytes = sizeof(float) * (size_t)(parts - 1) * BH * D * E;
+      if (off + sbytes <= max_ws_bytes && (parts - 1) * plen < n) {
+        plan->parts = parts;
+        plan->part_len = (int)plen;
+        plan->part_state_offset = off;
+        plan->partial_bytes = off + sbytes;
+      }
+    }
+  }
   return true;
 }
 
 hipError_t launch_prefill_feat(const void* q, const void* k, const void* v, void* y, int BH, int n, int dk, int dv,
                                int P, const DevTable& t, const FeatPrefillPlan& plan, float* S_state, float* partial,
                                hipStream_t s, int qg) {
+  // float32 inputs take split operands, bf16 inputs bf16 operands
+  auto launch = [&](const FeatLaunch& fl) {
+    return plan.split ? launch_main_nct<true, float>(plan, q, k, v, t, fl, partial, BH, n, dk, dv, qg, s)
+                      : launch_main_nct<false, u16>(plan, q, k, v, t, fl, partial, BH, n, dk, dv, qg, s);
+  };
   for (int seg0 = 0; seg0 < n; seg0 += plan.seg_len) {
-    const bool first = seg0 == 0;
-    // float32 inputs take split operands, bf16 inputs bf16 operands
-    hipError_t e = plan.split
-                       ? launch_main_nct<true, float>(plan, q, k, v, t, S_state, partial, BH, n, dk, dv, seg0, first,
-                                                      qg, s)
-                       : launch_main_nct<false, u16>(plan, q, k, v, t, S_state, partial, BH, n, dk, dv, seg0, first,
-                                                     qg, s);
+    hipError_t e;
+    if (plan.parts > 1) {  // (the call is one segment)
+      float* const Sp = (float*)((char*)partial + plan.part_state_offset);
+      e = launch(FeatLaunch{{nullptr, nullptr, nullptr, Sp}, seg0, plan.seg_len, plan.part_len, plan.parts - 1, false});
+      if (e != hipSuccess) return e;
+      if (plan.parts > 2) {
+        const int64_t count = (int64_t)BH * t.D * (dv + 1);
+        hipLaunchKernelGGL(prefix_part_states, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, Sp, count,
+                           plan.parts);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+      }
+      e = launch(FeatLaunch{{nullptr, Sp, S_state, nullptr}, seg0, plan.seg_len, plan.part_len, plan.parts, true});
+    } else {
+      const float* in0 = seg0 == 0 ? nullptr : S_state;
+      e = launch(FeatLaunch{{in0, nullptr, S_state, nullptr}, seg0, plan.seg_len, plan.seg_len, 1, true});
+    }
     if (e != hipSuccess) return e;
     if ((e = fold_slices(partial, plan, BH, n, dv, seg0, s)) != hipSuccess) return e;
     e = launch_prefill_generic_finalize(q, k, v, y, !plan.split, BH, n, dk, dv, P, kCh, 1, seg0, plan.seg_len, partial,
@@ -633,10 +710,9 @@ hipError_t launch_prefill_feat(const void* q, const void* k, const void* v, void
 hipError_t launch_prefill_feat_readout(const void* q, const void* k, const void* v, bool bf16_in, int BH, int n,
                                        int dk, int dv, const DevTable& t, const FeatPrefillPlan& plan,
                                        float* S_state, float* partial, int seg0, bool first, hipStream_t s) {
-  hipError_t e = bf16_in ? launch_main_nct<true, u16>(plan, q, k, v, t, S_state, partial, BH, n, dk, dv, seg0, first,
-                                                      1, s)
-                         : launch_main_nct<true, float>(plan, q, k, v, t, S_state, partial, BH, n, dk, dv, seg0,
-                                                        first, 1, s);
+  const FeatLaunch fl{{first ? nullptr : S_state, nullptr, S_state, nullptr}, seg0, plan.seg_len, plan.seg_len, 1, true};
+  hipError_t e = bf16_in ? launch_main_nct<true, u16>(plan, q, k, v, t, fl, partial, BH, n, dk, dv, 1, s)
+                         : launch_main_nct<true, float>(plan, q, k, v, t, fl, partial, BH, n, dk, dv, 1, s);
   if (e != hipSuccess) return e;
   return fold_slices(partial, plan, BH, n, dv, seg0, s);
 }

@@ -464,6 +464,19 @@ sata_status sata_prefill_operands(sata_dtype dt, int B, int H, int n, int d_k, i
   return ok();
 }
 
+sata_status sata_prefill_parts(sata_dtype dt, int B, int H, int n, int d_k, int d_v, int P, int chunk, int* parts) {
+  if (!parts) return fail(SATA_ERR_INVALID_ARG, "null output pointer");
+  int64_t D = 0;
+  sata_status st = check_prefill_args(dt, B, H, n, d_k, d_v, P, chunk, &D);
+  if (st != SATA_OK) return st;
+  *parts = 1;
+  sata::FeatPrefillPlan fp;
+  if (prefill_path(dt, B * H, n, d_k, d_v, P, chunk) == PrefillPath::kFeat &&
+      sata::plan_prefill_feat(D, B * H, n, d_k, d_v, P, chunk, dt == SATA_F32, kMaxFeatWorkspace, &fp))
+    *parts = fp.parts;
+  return ok();
+}
+
 sata_status sata_prefill(const void* q, const void* k, const void* v, sata_dtype dt, int B, int H, int n,
                          int d_k, int d_v, int P, int chunk, void* y, float* S_out, void* stream) {
   int64_t D = 0;

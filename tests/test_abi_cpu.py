@@ -155,6 +155,32 @@ def test_prefill_operands_query(lib):
     assert bnd.prefill_operands(torch.bfloat16, 1, 1, 100, 8, 8, 4, 64) == "bf16"
 
 
+def test_prefill_parts_query(lib):
+    out = ctypes.c_int(-1)
+    # the float32 sweep at P = 2 and 3 (64 heads of 17 / 153 features, one
+    # workgroup each): four parts of 16384 tokens fill the 256 compute units
+    assert lib.sata_prefill_parts(0, 1, 64, 65536, 16, 16, 2, 64, ctypes.byref(out)) == 0 and out.value == 4
+    assert lib.sata_prefill_parts(0, 1, 64, 65536, 16, 16, 3, 64, ctypes.byref(out)) == 0 and out.value == 4
+    # enough workgroups already (4 slices x 64 heads; 94 x 16 at d = 64): one scan
+    assert lib.sata_prefill_parts(0, 1, 64, 65536, 16, 16, 4, 64, ctypes.byref(out)) == 0 and out.value == 1
+    assert lib.sata_prefill_parts(1, 2, 8, 4096, 64, 64, 4, 64, ctypes.byref(out)) == 0 and out.value == 1
+    # parts keep at least 1024 tokens: two heads of 8192 tokens take 8, of 4096
+    # take 4, of 2047 two (1024 + 1023), of 1500 none
+    assert lib.sata_prefill_parts(0, 1, 2, 8192, 8, 8, 3, 64, ctypes.byref(out)) == 0 and out.value == 8
+    assert lib.sata_prefill_parts(1, 1, 2, 4096, 8, 8, 3, 64, ctypes.byref(out)) == 0 and out.value == 4
+    assert lib.sata_prefill_parts(1, 1, 2, 2047, 8, 8, 3, 64, ctypes.byref(out)) == 0 and out.value == 2
+    assert lib.sata_prefill_parts(1, 1, 2, 1500, 8, 8, 3, 64, ctypes.byref(out)) == 0 and out.value == 1
+    # one head, long sequence: at most 16 parts
+    assert lib.sata_prefill_parts(0, 1, 1, 1 << 20, 8, 8, 3, 64, ctypes.byref(out)) == 0 and out.value == 16
+    # other paths scan in one pass
+    assert lib.sata_prefill_parts(1, 1, 1, 8192, 32, 32, 4, 64, ctypes.byref(out)) == 0 and out.value == 1
+    assert lib.sata_prefill_parts(0, 1, 1, 8192, 8, 8, 4, 32, ctypes.byref(out)) == 0 and out.value == 1
+    assert lib.sata_prefill_parts(1, 1, 1, 8, 32, 32, 4, 48, ctypes.byref(out)) == -2
+    assert lib.sata_prefill_parts(1, 1, 1, 8, 32, 32, 4, 64, None) == -1
+    torch = pytest.importorskip("torch")
+    assert bnd.prefill_parts(torch.float32, 1, 64, 65536, 16, 16, 2) == 4
+
+
 class TestBindingRejectsBeforeLaunch:
     """The tensor wrappers check dtypes and shapes before anything reaches the
     library, so a mismatched output or input is refused instead of being

@@ -16,7 +16,7 @@ import pytest
 import oracle
 import sata_synth as syn
 from gpu_util import (check_prefill_head, check_rows, check_state, check_state_against, operands, to_dev, to_host,
-                      y_tol)
+                      torch_dtype, y_tol)
 from oracle.metrics import max_row_rel_error
 
 pytestmark = pytest.mark.gpu
@@ -138,6 +138,33 @@ def test_prefill_generated_features_matches_oracle(sata, case):
     ops = operands(sata, dtype, B, H, n, dk, dv, P, chunk)
     assert ops == ("bf16" if dtype == "bf16" else "split"), "expected on the matrix cores"
     q, k, v, y, S = _run_prefill(sata, *case)
+    for b in range(B):
+        for h in range(H):
+            check_prefill_head(y[b, h], S[b, h], q[b, h], k[b, h], v[b, h], P, ops, dtype, chunk,
+                               f"{case} b{b} h{h}")
+
+
+# Few heads with few features over a long sequence: the sequence is cut into
+# parts that run side by side, each starting from the summed state increments
+# of the parts before it (sata_prefill_parts); every row and the final state
+# against the oracle.
+SPLIT_CASES = [
+    # workload, B, H, n, d_k, d_v, P, chunk, dtype, parts
+    (55, 1, 2, 8192, 8, 8, 3, 64, "f32", 8),
+    (56, 1, 1, 4150, 16, 16, 2, 64, "bf16", 4),
+    (57, 2, 1, 3000, 5, 3, 4, 64, "f32", 2),
+    (58, 1, 1, 2100, 24, 48, 3, 64, "bf16", 2),
+]
+
+
+@pytest.mark.parametrize("case", SPLIT_CASES, ids=lambda c: "w{}_B{}H{}n{}dk{}dv{}P{}C{}_{}_parts{}".format(*c))
+def test_prefill_split_sequence_matches_oracle(sata, case):
+    *args, parts = case
+    workload, B, H, n, dk, dv, P, chunk, dtype = args
+    _say(f"prefill (sequence in parts) {case}")
+    assert sata.prefill_parts(torch_dtype(dtype), B, H, n, dk, dv, P, chunk) == parts
+    ops = operands(sata, dtype, B, H, n, dk, dv, P, chunk)
+    q, k, v, y, S = _run_prefill(sata, *args)
     for b in range(B):
         for h in range(H):
             check_prefill_head(y[b, h], S[b, h], q[b, h], k[b, h], v[b, h], P, ops, dtype, chunk,
