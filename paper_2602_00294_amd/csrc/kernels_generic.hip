@@ -681,10 +681,13 @@ prefill_generic_finalize(const T* __restrict__ q, const T* __restrict__ k, const
       const int r = o / E;
       const int j = o - r * E;
       const int t = rb + r;
+      const float* const pr = part + ((int64_t)bh * seg_len + (t0 - seg0) + t) * E + j;
+      const int64_t sstride = (int64_t)BH * seg_len * E;
+      const float p0 = nslices > 0 ? pr[0] : 0.0f;  // issued before the sum below
       float acc = 0.0f;
       for (int tp = 0; tp <= t; ++tp) acc += A[r * C + tp] * ve[tp * E + j];
-      for (int s = 0; s < nslices; ++s)
-        acc += part[(((int64_t)s * BH + bh) * seg_len + (t0 - seg0) + t) * E + j];
+      acc += p0;
+      for (int s = 1; s < nslices; ++s) acc += pr[s * sstride];
       O[o] = acc;
     }
     __syncthreads();
