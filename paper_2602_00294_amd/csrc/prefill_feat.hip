@@ -533,6 +533,119 @@ __global__ void __launch_bounds__(256) reduce_slices(float* __restrict__ part, i
   part[off] = a;
 }
 
+// ---- finalize: the intra-chunk term and the division (App. A2: within a
+// chunk the causal attention weights are the truncated Taylor polynomial of
+// q.k / sqrt(d_k) itself).  One workgroup of 4 waves per (chunk of 64 tokens,
+// head); wave w owns query rows 16 w .. 16 w + 15.  Both products run on
+// v_mfma_f32_16x16x4_f32 (float32 operands and accumulation):
+//   W[t][t'] = f_P(q_t . k_t' / sqrt(d_k)) for t' <= t, else 0   (Q K^T tiles)
+//   O = partial + W [V | 1],   y_t = O[t][0:d_v] / O[t][d_v].
+// Operand layouts (16 x 16 x 4 f32): A lane l holds row l % 16, K entry l / 16;
+// B lane l holds column l % 16, K row l / 16; the result lane l holds column
+// l % 16, rows 4 (l / 16) .. +3.  Each wave reads and writes only its own rows
+// of W and O, so no barrier separates the steps after the loads.
+constexpr int kFinWS = 68;  // floats per row of W (64 + 4: the A reads hit distinct banks)
+__host__ __device__ constexpr int fin_xq(int dk) { return (dk + 7) / 8 * 8 + 4; }
+__host__ __device__ constexpr int fin_ep(int dv) { return (dv + 1 + 15) / 16 * 16; }
+__host__ __device__ constexpr int fin_vs(int dv) { return fin_ep(dv) | 16; }
+inline size_t fin_lds_bytes(int dk, int dv) {
+  return sizeof(float) * ((size_t)2 * kCh * fin_xq(dk) + (size_t)2 * kCh * fin_vs(dv) + (size_t)kCh * kFinWS);
+}
+
+__device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) feat_finalize(const T* __restrict__ q, const T* __restrict__ k,
+                                                     const T* __restrict__ v, const float* __restrict__ part,
+                                                     T* __restrict__ y, int n, int dk, int dv, int P, int seg0,
+                                                     int seg_len, int qg) {
+  extern __shared__ __attribute__((aligned(16))) float flds[];
+  const int E = dv + 1;
+  const int XQ = fin_xq(dk), EP = fin_ep(dv), VS = fin_vs(dv);
+  float* const xq = flds;           // [64][XQ], zero past d_k and past the sequence
+  float* const xk = xq + kCh * XQ;  // [64][XQ]
+  float* const v1 = xk + kCh * XQ;  // [64][VS]: [V | 1], zero past E and past the sequence
+  float* const W = v1 + kCh * VS;   // [64][kFinWS]
+  float* const O = W + kCh * kFinWS;  // [64][VS]
+  const int64_t bh = blockIdx.y;
+  const int t0 = seg0 + blockIdx.x * kCh;
+  if (t0 >= n) return;
+  const int cn = min(kCh, n - t0);
+  const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, l4 = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int dk4 = (dk + 3) & ~3;
+  const T* const qh = q + (bh * qg * n + t0) * (int64_t)dk;
+  const T* const kh = k + (bh * n + t0) * (int64_t)dk;
+  const T* const vh = v + (bh * n + t0) * (int64_t)dv;
+  for (int i = tid; i < kCh * dk4; i += 256) {
+    const int t = i / dk4, c = i - t * dk4;
+    const bool in = t < cn && c < dk;
+    xq[t * XQ + c] = in ? to_f32(qh[t * dk + c]) : 0.f;
+    xk[t * XQ + c] = in ? to_f32(kh[t * dk + c]) : 0.f;
+  }
+  for (int i = tid; i < kCh * EP; i += 256) {
+    const int t = i / EP, c = i - t * EP;
+    float val = 0.f;
+    if (t < cn) val = c < dv ? to_f32(vh[t * dv + c]) : (c == dv ? 1.f : 0.f);
+    v1[t * VS + c] = val;
+  }
+  __syncthreads();
+  const float scale = 1.0f / sqrtf((float)dk);
+  const int r0 = 16 * wave;  // this wave's rows
+  for (int nt = 0; nt <= wave; ++nt) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int kk = 0; kk < dk4; kk += 4)
+      acc = mfma4(xq[(r0 + l16) * XQ + kk + l4], xk[(16 * nt + l16) * XQ + kk + l4], acc);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = r0 + 4 * l4 + i, tp = 16 * nt + l16;
+      W[t * kFinWS + tp] = tp <= t ? taylor_horner(acc[i] * scale, P) : 0.f;
+    }
+  }
+  const float* const pr = part + ((int64_t)bh * seg_len + (t0 - seg0)) * E;
+  for (int jt = 0; jt < EP / 16; ++jt) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int kk = 0; kk < r0 + 16; kk += 4)
+      acc = mfma4(W[(r0 + l16) * kFinWS + kk + l4], v1[(kk + l4) * VS + 16 * jt + l16], acc);
+    const int c = 16 * jt + l16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = r0 + 4 * l4 + i;
+      O[t * VS + c] = acc[i] + ((c < E && t < cn) ? pr[(int64_t)t * E + c] : 0.f);
+    }
+  }
+  for (int i = lane; i < 16 * dv; i += 64) {
+    const int r = i / dv, j = i - r * dv;
+    const int t = r0 + r;
+    if (t < cn) y[(bh * qg * n + t0 + t) * (int64_t)dv + j] = from_f32<T>(O[t * VS + j] / O[t * VS + dv]);
+  }
+}
+
+hipError_t launch_feat_finalize(const void* q, const void* k, const void* v, void* y, bool bf16, int BH, int n,
+                                int dk, int dv, int P, int seg0, int seg_len, const float* partial, hipStream_t s,
+                                int qg) {
+  const size_t lds = fin_lds_bytes(dk, dv);
+  const int seg_tokens = std::min(seg_len, n - seg0);
+  const dim3 grid((unsigned)((seg_tokens + kCh - 1) / kCh), (unsigned)BH);
+  hipError_t e;
+  if (bf16) {
+    if ((e = hipFuncSetAttribute((const void*)feat_finalize<bf16_t>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)lds)) != hipSuccess)
+      return e;
+    hipLaunchKernelGGL(feat_finalize<bf16_t>, grid, dim3(256), lds, s, (const bf16_t*)q, (const bf16_t*)k,
+                       (const bf16_t*)v, partial, (bf16_t*)y, n, dk, dv, P, seg0, seg_len, qg);
+  } else {
+    if ((e = hipFuncSetAttribute((const void*)feat_finalize<float>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)lds)) != hipSuccess)
+      return e;
+    hipLaunchKernelGGL(feat_finalize<float>, grid, dim3(256), lds, s, (const float*)q, (const float*)k,
+                       (const float*)v, partial, (float*)y, n, dk, dv, P, seg0, seg_len, qg);
+  }
+  return hipGetLastError();
+}
+
 // Tiles of 16 features per wave for NCT column tiles: the state, the readout
 // sums (4 x NCT tiles) and the generation's registers fit two waves per SIMD.
 constexpr int ft_for(int nct, bool x3) {
@@ -700,8 +813,7 @@ hipError_t launch_prefill_feat(const void* q, const void* k, const void* v, void
     }
     if (e != hipSuccess) return e;
     if ((e = fold_slices(partial, plan, BH, n, dv, seg0, s)) != hipSuccess) return e;
-    e = launch_prefill_generic_finalize(q, k, v, y, !plan.split, BH, n, dk, dv, P, kCh, 1, seg0, plan.seg_len, partial,
-                                        s, qg);
+    e = launch_feat_finalize(q, k, v, y, !plan.split, BH, n, dk, dv, P, seg0, plan.seg_len, partial, s, qg);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
