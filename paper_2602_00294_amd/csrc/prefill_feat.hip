@@ -545,15 +545,46 @@ __global__ void __launch_bounds__(256) reduce_slices(float* __restrict__ part, i
 // l % 16, rows 4 (l / 16) .. +3.  Each wave reads and writes only its own rows
 // of W and O, so no barrier separates the steps after the loads.
 constexpr int kFinWS = 68;  // floats per row of W (64 + 4: the A reads hit distinct banks)
+constexpr int kFinMaxNT = 5;  // column tiles of 16 covering d_v + 1 <= 65
 __host__ __device__ constexpr int fin_xq(int dk) { return (dk + 7) / 8 * 8 + 4; }
 __host__ __device__ constexpr int fin_ep(int dv) { return (dv + 1 + 15) / 16 * 16; }
 __host__ __device__ constexpr int fin_vs(int dv) { return fin_ep(dv) | 16; }
 inline size_t fin_lds_bytes(int dk, int dv) {
-  return sizeof(float) * ((size_t)2 * kCh * fin_xq(dk) + (size_t)2 * kCh * fin_vs(dv) + (size_t)kCh * kFinWS);
+  return sizeof(float) * ((size_t)2 * kCh * fin_xq(dk) + (size_t)kCh * fin_vs(dv) + (size_t)kCh * kFinWS);
 }
 
 __device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// rows [0, 64) of a chunk (rows of `width` elements, contiguous in src, zero
+// past row cn) into float32 LDS rows of `stride`; 16-byte loads where the
+// rows allow them
+template <typename T>
+__device__ __forceinline__ void fin_load_rows(const T* __restrict__ src, int width, int cn, float* dst, int stride,
+                                              bool vec) {
+  constexpr int kEV = 16 / sizeof(T);
+  if (vec) {
+    const int per = width / kEV;
+    for (int i = threadIdx.x; i < kCh * per; i += 256) {
+      const int t = i / per, c = (i - t * per) * kEV;
+      uint4 w = {0u, 0u, 0u, 0u};
+      if (t < cn) w = *(const uint4*)(src + (int64_t)t * width + c);
+      const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int j = 0; j < kEV; ++j) {
+        float f;
+        if constexpr (sizeof(T) == 4) f = __uint_as_float(u[j]);
+        else f = __uint_as_float(j & 1 ? u[j >> 1] & 0xffff0000u : u[j >> 1] << 16);
+        dst[t * stride + c + j] = f;
+      }
+    }
+  } else {
+    for (int i = threadIdx.x; i < kCh * width; i += 256) {
+      const int t = i / width, c = i - t * width;
+      dst[t * stride + c] = t < cn ? to_f32(src[(int64_t)t * width + c]) : 0.f;
+    }
+  }
 }
 
 template <typename T>
@@ -563,37 +594,50 @@ __global__ void __launch_bounds__(256) feat_finalize(const T* __restrict__ q, co
                                                      int seg_len, int qg) {
   extern __shared__ __attribute__((aligned(16))) float flds[];
   const int E = dv + 1;
-  const int XQ = fin_xq(dk), EP = fin_ep(dv), VS = fin_vs(dv);
+  const int XQ = fin_xq(dk), EP = fin_ep(dv), VS = fin_vs(dv), NT = EP / 16;
   float* const xq = flds;           // [64][XQ], zero past d_k and past the sequence
   float* const xk = xq + kCh * XQ;  // [64][XQ]
   float* const v1 = xk + kCh * XQ;  // [64][VS]: [V | 1], zero past E and past the sequence
   float* const W = v1 + kCh * VS;   // [64][kFinWS]
-  float* const O = W + kCh * kFinWS;  // [64][VS]
   const int64_t bh = blockIdx.y;
   const int t0 = seg0 + blockIdx.x * kCh;
   if (t0 >= n) return;
   const int cn = min(kCh, n - t0);
   const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, l4 = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int dk4 = (dk + 3) & ~3;
+  const int r0 = 16 * wave;  // this wave's rows
   const T* const qh = q + (bh * qg * n + t0) * (int64_t)dk;
   const T* const kh = k + (bh * n + t0) * (int64_t)dk;
   const T* const vh = v + (bh * n + t0) * (int64_t)dv;
-  for (int i = tid; i < kCh * dk4; i += 256) {
-    const int t = i / dk4, c = i - t * dk4;
-    const bool in = t < cn && c < dk;
-    xq[t * XQ + c] = in ? to_f32(qh[t * dk + c]) : 0.f;
-    xk[t * XQ + c] = in ? to_f32(kh[t * dk + c]) : 0.f;
+  // the partial sums of this wave's results (rows r0 + 4 l4 + i, column
+  // 16 jt + l16), fetched first so that they arrive during the rest
+  const float* const pr = part + ((int64_t)bh * seg_len + (t0 - seg0)) * E;
+  float pp[kFinMaxNT][4];
+#pragma unroll
+  for (int jt = 0; jt < kFinMaxNT; ++jt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = r0 + 4 * l4 + i, c = 16 * jt + l16;
+      pp[jt][i] = (jt < NT && c < E && t < cn) ? pr[(int64_t)t * E + c] : 0.f;
+    }
+  constexpr int kEV = 16 / sizeof(T);
+  const bool vq = dk % kEV == 0 && (((uintptr_t)qh | (uintptr_t)kh) & 15) == 0;
+  const bool vv = dv % kEV == 0 && ((uintptr_t)vh & 15) == 0;
+  fin_load_rows(qh, dk, cn, xq, XQ, vq);
+  fin_load_rows(kh, dk, cn, xk, XQ, vq);
+  fin_load_rows(vh, dv, cn, v1, VS, vv);
+  const int dk4 = (dk + 3) & ~3;
+  for (int i = tid; i < kCh * (dk4 - dk); i += 256) {  // zero K padding
+    const int t = i / (dk4 - dk), c = dk + i - t * (dk4 - dk);
+    xq[t * XQ + c] = 0.f;
+    xk[t * XQ + c] = 0.f;
   }
-  for (int i = tid; i < kCh * EP; i += 256) {
-    const int t = i / EP, c = i - t * EP;
-    float val = 0.f;
-    if (t < cn) val = c < dv ? to_f32(vh[t * dv + c]) : (c == dv ? 1.f : 0.f);
-    v1[t * VS + c] = val;
+  for (int i = tid; i < kCh * (EP - dv); i += 256) {  // the 1 column and zero padding
+    const int t = i / (EP - dv), c = dv + i - t * (EP - dv);
+    v1[t * VS + c] = (c == dv && t < cn) ? 1.f : 0.f;
   }
   __syncthreads();
   const float scale = 1.0f / sqrtf((float)dk);
-  const int r0 = 16 * wave;  // this wave's rows
   for (int nt = 0; nt <= wave; ++nt) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int kk = 0; kk < dk4; kk += 4)
@@ -604,22 +648,36 @@ __global__ void __launch_bounds__(256) feat_finalize(const T* __restrict__ q, co
       W[t * kFinWS + tp] = tp <= t ? taylor_horner(acc[i] * scale, P) : 0.f;
     }
   }
-  const float* const pr = part + ((int64_t)bh * seg_len + (t0 - seg0)) * E;
-  for (int jt = 0; jt < EP / 16; ++jt) {
+  auto out_tile = [&](int jt) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int kk = 0; kk < r0 + 16; kk += 4)
       acc = mfma4(W[(r0 + l16) * kFinWS + kk + l4], v1[(kk + l4) * VS + 16 * jt + l16], acc);
+    return acc;
+  };
+  // the normaliser column first: every lane takes its rows' normalisers from
+  // the lane of its row group that holds column d_v
+  const int jn = dv >> 4;
+  f32x4 accn = out_tile(jn);
+  float z[4];
+#pragma unroll
+  for (int jt = 0; jt < kFinMaxNT; ++jt)
+    if (jt == jn)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) accn[i] += pp[jt][i];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) z[i] = __shfl(accn[i], 16 * l4 + (dv & 15));
+  T* const yh = y + (bh * qg * n + t0) * (int64_t)dv;
+#pragma unroll
+  for (int jt = 0; jt < kFinMaxNT; ++jt) {
+    if (jt >= NT) break;
+    f32x4 acc = jt == jn ? accn : out_tile(jt);
     const int c = 16 * jt + l16;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int t = r0 + 4 * l4 + i;
-      O[t * VS + c] = acc[i] + ((c < E && t < cn) ? pr[(int64_t)t * E + c] : 0.f);
+      if (jt != jn) acc[i] += pp[jt][i];
+      if (c < dv && t < cn) yh[(int64_t)t * dv + c] = from_f32<T>(acc[i] / z[i]);
     }
-  }
-  for (int i = lane; i < 16 * dv; i += 64) {
-    const int r = i / dv, j = i - r * dv;
-    const int t = r0 + r;
-    if (t < cn) y[(bh * qg * n + t0 + t) * (int64_t)dv + j] = from_f32<T>(O[t * VS + j] / O[t * VS + dv]);
   }
 }
 
