@@ -401,8 +401,12 @@ backward_dkv_main(const T* __restrict__ q, const T* __restrict__ k, const T* __r
 
 // Intra-chunk weights of one chunk into LDS: for query row r and key column c
 // (c <= r), W[r][c] = f_P(s_rc) and G[r][c] = (h_r . [v_c|1]) f_{P-1}(s_rc) / sqrt(d_k).
+// Row stride of the coordinates in the intra-chunk kernels: odd, so that lanes
+// that read different key rows at one coordinate hit different LDS banks.
+__host__ __device__ constexpr int bw_fin_stride(int dk) { return dk | 1; }
+
 __device__ void bw_intra_weights(const float* xq, const float* xk, const float* ve, const float* hh, int cn, int C,
-                                 int dk, int E, int P, float* W, float* Gm) {
+                                 int dk, int XS, int E, int P, float* W, float* Gm) {
   const float scale = 1.0f / sqrtf((float)dk);
   for (int i = threadIdx.x; i < C * C; i += blockDim.x) {
     const int r = i / C;
@@ -410,7 +414,7 @@ __device__ void bw_intra_weights(const float* xq, const float* xk, const float* 
     float w = 0.0f, g = 0.0f;
     if (r < cn && c <= r) {
       float dot = 0.0f;
-      for (int a = 0; a < dk; ++a) dot += xq[r * dk + a] * xk[c * dk + a];
+      for (int a = 0; a < dk; ++a) dot += xq[r * XS + a] * xk[c * XS + a];
       const float sc = dot * scale;
       float hv = 0.0f;
       for (int j = 0; j < E; ++j) hv += hh[r * E + j] * ve[c * E + j];
@@ -431,8 +435,10 @@ backward_h_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* _
   extern __shared__ __attribute__((aligned(16))) float lds[];
   const int E = dv + 1;
   float* xq = lds;
-  float* xk = xq + C * dk;
-  float* ve = xk + C * dk;
+  // odd row stride: the lanes of the Q K^T loop read different key rows
+  const int XS = bw_fin_stride(dk);
+  float* xk = xq + C * XS;
+  float* ve = xk + C * XS;
   float* O = ve + C * E;   // [C][E]
   float* W = O + C * E;    // [C][C]
   const int64_t bh = blockIdx.y;
@@ -444,8 +450,9 @@ backward_h_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* _
   const int64_t off = (bh * n + t0) * (int64_t)dk;
   for (int i = tid; i < C * dk; i += blockDim.x) {
     const int t = i / dk;
-    xq[i] = t < cn ? to_f32(q[off + i]) : 0.0f;
-    xk[i] = t < cn ? to_f32(k[off + i]) : 0.0f;
+    const int a = i - t * dk;
+    xq[t * XS + a] = t < cn ? to_f32(q[off + i]) : 0.0f;
+    xk[t * XS + a] = t < cn ? to_f32(k[off + i]) : 0.0f;
   }
   for (int i = tid; i < C * E; i += blockDim.x) {
     const int t = i / E;
@@ -459,7 +466,7 @@ backward_h_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* _
     float w = 0.0f;
     if (r < cn && c <= r) {
       float dot = 0.0f;
-      for (int a = 0; a < dk; ++a) dot += xq[r * dk + a] * xk[c * dk + a];
+      for (int a = 0; a < dk; ++a) dot += xq[r * XS + a] * xk[c * XS + a];
       w = taylor_horner(dot * scale, P);
     }
     W[i] = w;
@@ -494,8 +501,9 @@ backward_dq_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* 
   extern __shared__ __attribute__((aligned(16))) float lds[];
   const int E = dv + 1;
   float* xq = lds;
-  float* xk = xq + C * dk;
-  float* ve = xk + C * dk;
+  const int XS = bw_fin_stride(dk);
+  float* xk = xq + C * XS;
+  float* ve = xk + C * XS;
   float* hh = ve + C * E;
   float* W = hh + C * E;
   float* Gm = W + C * C;
@@ -503,15 +511,15 @@ backward_dq_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* 
   const int t0 = seg0 + blockIdx.x * C;
   if (t0 >= n) return;
   const int cn = min(C, n - t0);
-  bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh, dk);
+  bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh, XS);
   __syncthreads();
-  bw_intra_weights(xq, xk, ve, hh, cn, C, dk, E, P, W, Gm);
+  bw_intra_weights(xq, xk, ve, hh, cn, C, dk, XS, E, P, W, Gm);
   __syncthreads();
   for (int i = threadIdx.x; i < cn * dk; i += blockDim.x) {
     const int r = i / dk;
     const int a = i - r * dk;
     float acc = 0.0f;
-    for (int c = 0; c <= r; ++c) acc += Gm[r * C + c] * xk[c * dk + a];
+    for (int c = 0; c <= r; ++c) acc += Gm[r * C + c] * xk[c * XS + a];
     for (int s = 0; s < nslices; ++s) acc += part[(((int64_t)s * BH + bh) * seg_len + (t0 - seg0) + r) * dk + a];
     dq[(bh * n + t0 + r) * (int64_t)dk + a] = from_f32<T>(acc);
   }
@@ -528,8 +536,9 @@ backward_dkv_finalize(const T* __restrict__ q, const T* __restrict__ k, const T*
   const int E = dv + 1;
   const int PW = dk + dv;
   float* xq = lds;
-  float* xk = xq + C * dk;
-  float* ve = xk + C * dk;
+  const int XS = bw_fin_stride(dk);
+  float* xk = xq + C * XS;
+  float* ve = xk + C * XS;
   float* hh = ve + C * E;
   float* W = hh + C * E;
   float* Gm = W + C * C;
@@ -537,16 +546,16 @@ backward_dkv_finalize(const T* __restrict__ q, const T* __restrict__ k, const T*
   const int t0 = seg0 + blockIdx.x * C;
   if (t0 >= n) return;
   const int cn = min(C, n - t0);
-  bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh, dk);
+  bw_load_chunk(q, k, v, h, bh, n, t0, cn, C, dk, dv, xq, xk, ve, hh, XS);
   __syncthreads();
-  bw_intra_weights(xq, xk, ve, hh, cn, C, dk, E, P, W, Gm);
+  bw_intra_weights(xq, xk, ve, hh, cn, C, dk, XS, E, P, W, Gm);
   __syncthreads();
   for (int i = threadIdx.x; i < cn * PW; i += blockDim.x) {
     const int c = i / PW;
     const int a = i - c * PW;
     float acc = 0.0f;
     if (a < dk) {
-      for (int r = c; r < cn; ++r) acc += Gm[r * C + c] * xq[r * dk + a];
+      for (int r = c; r < cn; ++r) acc += Gm[r * C + c] * xq[r * XS + a];
     } else {
       for (int r = c; r < cn; ++r) acc += W[r * C + c] * hh[r * E + (a - dk)];
     }
@@ -584,8 +593,8 @@ bool plan_backward(int64_t D, int BH, int n, int dk, int dv, int P, int chunk, s
   plan->fs = (int)fs;
   plan->nslices = (int)((D + fs - 1) / fs);
   plan->lds_main = sizeof(float) * L.floats();
-  plan->lds_h = sizeof(float) * (2 * (size_t)C * dk + 2 * (size_t)C * E + (size_t)C * C);
-  plan->lds_fin = sizeof(float) * (2 * (size_t)C * dk + 2 * (size_t)C * E + 2 * (size_t)C * C);
+  plan->lds_h = sizeof(float) * (2 * (size_t)C * bw_fin_stride(dk) + 2 * (size_t)C * E + (size_t)C * C);
+  plan->lds_fin = sizeof(float) * (2 * (size_t)C * bw_fin_stride(dk) + 2 * (size_t)C * E + 2 * (size_t)C * C);
   // partial rows per token: the forward readout (E per forward slice), dq (dk),
   // dk and dv (dk + dv) per backward slice
   const size_t fwd_slices = plan->feat_fwd ? (size_t)plan->feat.nslices : (size_t)fwd->nslices;
