@@ -10,7 +10,7 @@ import pytest
 
 import oracle
 import sata_synth as syn
-from gpu_util import check_rows, check_state, operands, to_dev, to_host, y_tol
+from gpu_util import check_rows, check_state, operands, to_dev, to_host, torch_dtype, y_tol
 
 pytestmark = pytest.mark.gpu
 
@@ -99,6 +99,7 @@ def test_grouped_decode_deterministic_and_g1_is_decode_step(sata):
     (1, 3, 2, 100, 8, 3, 64, "bf16"),    # the generated-feature matrix-core kernel
     (1, 3, 2, 70, 8, 4, 64, "f32"),      # the float32 kernel
     (1, 1, 8, 40, 5, 3, 16, "f32"),
+    (1, 1, 2, 4096, 8, 3, 64, "f32"),    # the generated-feature kernel, sequence in 4 parts
 ])
 def test_grouped_prefill_matches_oracle(sata, B, Hkv, G, n, d, P, chunk, dtype):
     """Every query head's rows against the oracle applied to its own queries and
@@ -112,6 +113,8 @@ def test_grouped_prefill_matches_oracle(sata, B, Hkv, G, n, d, P, chunk, dtype):
     y, S = sata.prefill_grouped(qd, kd, vd, P, chunk)
     torch.cuda.synchronize()
     ops = operands(sata, dtype, B, Hkv, n, d, d, P, chunk)
+    if n >= 4096:
+        assert sata.prefill_parts(torch_dtype(dtype), B, Hkv, n, d, d, P, chunk) == 4
     yh = to_host(y)
     for b in range(B):
         for hq in range(Hkv * G):
