@@ -401,6 +401,21 @@ backward_dkv_main(const T* __restrict__ q, const T* __restrict__ k, const T* __r
 
 // Intra-chunk weights of one chunk into LDS: for query row r and key column c
 // (c <= r), W[r][c] = f_P(s_rc) and G[r][c] = (h_r . [v_c|1]) f_{P-1}(s_rc) / sqrt(d_k).
+// a + p[0] + p[stride] + ... + p[(ns - 1) stride], added in that order, with
+// eight of the loads in flight at a time.
+__device__ __forceinline__ float add_slices(float a, const float* __restrict__ p, int64_t stride, int ns) {
+  int s = 0;
+  for (; s + 8 <= ns; s += 8) {
+    float x[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) x[u] = p[(s + u) * stride];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) a += x[u];
+  }
+  for (; s < ns; ++s) a += p[s * stride];
+  return a;
+}
+
 // Row stride of the coordinates in the intra-chunk kernels: odd, so that lanes
 // that read different key rows at one coordinate hit different LDS banks.
 __host__ __device__ constexpr int bw_fin_stride(int dk) { return dk | 1; }
@@ -477,7 +492,7 @@ backward_h_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* _
     const int j = o - r * E;
     float acc = 0.0f;
     for (int c = 0; c <= r; ++c) acc += W[r * C + c] * ve[c * E + j];
-    for (int s = 0; s < nslices; ++s) acc += part[(((int64_t)s * BH + bh) * seg_len + (t0 - seg0) + r) * E + j];
+    acc = add_slices(acc, part + ((int64_t)bh * seg_len + (t0 - seg0) + r) * E + j, (int64_t)BH * seg_len * E, nslices);
     O[o] = acc;
   }
   __syncthreads();
@@ -520,7 +535,7 @@ backward_dq_finalize(const T* __restrict__ q, const T* __restrict__ k, const T* 
     const int a = i - r * dk;
     float acc = 0.0f;
     for (int c = 0; c <= r; ++c) acc += Gm[r * C + c] * xk[c * XS + a];
-    for (int s = 0; s < nslices; ++s) acc += part[(((int64_t)s * BH + bh) * seg_len + (t0 - seg0) + r) * dk + a];
+    acc = add_slices(acc, part + ((int64_t)bh * seg_len + (t0 - seg0) + r) * dk + a, (int64_t)BH * seg_len * dk, nslices);
     dq[(bh * n + t0 + r) * (int64_t)dk + a] = from_f32<T>(acc);
   }
 }
@@ -559,7 +574,7 @@ backward_dkv_finalize(const T* __restrict__ q, const T* __restrict__ k, const T*
     } else {
       for (int r = c; r < cn; ++r) acc += W[r * C + c] * hh[r * E + (a - dk)];
     }
-    for (int s = 0; s < nslices; ++s) acc += part[(((int64_t)s * BH + bh) * seg_len + (t0 - seg0) + c) * PW + a];
+    acc = add_slices(acc, part + ((int64_t)bh * seg_len + (t0 - seg0) + c) * PW + a, (int64_t)BH * seg_len * PW, nslices);
     if (a < dk)
       dk_out[(bh * n + t0 + c) * (int64_t)dk + a] = from_f32<T>(acc);
     else
