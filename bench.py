@@ -317,13 +317,19 @@ def run_workload(args, sata, torch):
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline_workload(wid, Bw, Hw, n, d, Ps, dt, y if len(Ps) == 1 else None,
                                                      pre if len(Ps) > 1 else None, sata, torch)
+        for Pw, e in line["cpu_baseline"]["per_P"].items():
+            if "gpu_log10_abs_diff_vs_softmax" in e:
+                per_P[Pw]["error_vs_softmax"] = {
+                    "measure": "log10 |y_gpu - y_softmax| elementwise (float64 exact softmax)",
+                    "rows": line["cpu_baseline"]["sample"], **e["gpu_log10_abs_diff_vs_softmax"]}
     return line
 
 
 def cpu_baseline_workload(wid, Bw, Hw, n, d, Ps, dt, y_gpu, pre, sata, torch):
     """The oracle on two heads of the workload: its rate on a bounded row sample,
     the GPU output's error against it on those rows and, for the sweep, the
-    error of the P-term method against exact softmax attention per P."""
+    error against exact softmax attention per P (of the GPU output, and of the
+    oracle's float64 P-term output on the same rows)."""
     import numpy as np
 
     import oracle
@@ -335,6 +341,11 @@ def cpu_baseline_workload(wid, Bw, Hw, n, d, Ps, dt, y_gpu, pre, sata, torch):
            "sample": f"rows {rows[0]}..{rows[-1]} ({len(rows)} rows) of heads {heads}, direct float64 definition"}
     t = 0.0
     per_P = {}
+    soft = {}  # exact softmax rows per head (independent of P)
+    if len(Ps) > 1:
+        for (b, h) in heads:
+            q, k, v = syn.make_head(wid, b, h, n, d, d, dt)
+            soft[(b, h)] = oracle.softmax_attention_rows(q, k, v, rows)
     for Pw in Ps:
         if y_gpu is None:  # the sweep: run each P again to have its output
             yP, _ = sata.prefill(*pre, Pw, CHUNK, want_state=False)
@@ -342,21 +353,25 @@ def cpu_baseline_workload(wid, Bw, Hw, n, d, Ps, dt, y_gpu, pre, sata, torch):
         else:
             yP = y_gpu
         yh = yP.float().cpu().numpy()
-        errs, lds = [], []
+        errs, lds, lds_gpu = [], [], []
         for (b, h) in heads:
             q, k, v = syn.make_head(wid, b, h, n, d, d, dt)
             t0 = time.perf_counter()
             yr, _, kap = oracle.taylor_attention_rows(q, k, v, Pw, rows)
             t += time.perf_counter() - t0
             errs.append(oracle.max_row_rel_error(yh[b, h, rows], yr, kap)[0])
-            if len(Ps) > 1:
-                lds.append(oracle.log10_abs_diff(yr, oracle.softmax_attention_rows(q, k, v, rows)))
+            if soft:
+                lds.append(oracle.log10_abs_diff(yr, soft[(b, h)]))
+                lds_gpu.append(oracle.log10_abs_diff(yh[b, h, rows], soft[(b, h)]))
         entry = {"parity_max_row_rel_err": max(errs)}
-        if lds:
-            a = np.concatenate([x.ravel() for x in lds])
+
+        def summary(parts):
+            a = np.concatenate([x.ravel() for x in parts])
             a = a[np.isfinite(a)]
-            entry["log10_abs_diff_vs_softmax"] = {"median": float(np.median(a)), "p99": float(np.percentile(a, 99)),
-                                                  "max": float(a.max())}
+            return {"median": float(np.median(a)), "p99": float(np.percentile(a, 99)), "max": float(a.max())}
+        if lds:
+            entry["gpu_log10_abs_diff_vs_softmax"] = summary(lds_gpu)
+            entry["log10_abs_diff_vs_softmax"] = summary(lds)
         per_P[str(Pw)] = entry
     out["value"] = len(heads) * len(rows) * len(Ps) / t / Hw
     out["seconds"] = t
