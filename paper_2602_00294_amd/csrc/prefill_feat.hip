@@ -711,12 +711,12 @@ hipError_t launch_feat_finalize(const void* q, const void* k, const void* v, voi
 
 // Tiles of 16 features per wave for NCT column tiles: the state, the readout
 // sums (4 x NCT tiles) and the generation's registers fit two waves per SIMD
-// (at NCT = 5 with bf16 operands, 6 tiles spill a few registers yet beat 4:
-// a third fewer slices, so less cross-wave reduction and fewer partial rows
-// per feature; 8 spill heavily).
+// (with bf16 operands, measured: 6 tiles at NCT = 5 spill a few registers yet
+// beat 4 (a third fewer slices, so less cross-wave reduction and fewer
+// partial rows per feature; 8 spill heavily), and 6 beat 8 and 10 at NCT = 3).
 constexpr int ft_for(int nct, bool x3) {
   return x3 ? (nct <= 1 ? 22 : nct == 2 ? 10 : nct == 3 ? 6 : nct == 4 ? 4 : 2)
-            : (nct <= 1 ? 28 : nct == 2 ? 16 : nct == 3 ? 8 : nct == 4 ? 6 : 6);
+            : (nct <= 1 ? 28 : nct == 2 ? 16 : nct == 3 ? 6 : nct == 4 ? 6 : 6);
 }
 // Tiles per wave of the narrow variant: slices of 256 features, for heads
 // whose few features would otherwise leave most waves, or most compute
