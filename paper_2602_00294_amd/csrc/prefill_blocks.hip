@@ -766,7 +766,11 @@ std::map<std::pair<int, int>, DeviceTables> g_mfma_tables;  // (device, dk)
 
 constexpr int kNW = 8;
 
-int ppw_for(int dk) { return dk == 16 ? 16 : 8; }
+// Pairs per wave.  At d = 16, 6 (measured against 4, 8, 10, 12, 14, 16: fewer
+// state registers per wave, so more workgroups resident, outweigh the extra
+// slices' partial rows; 16 took 2.26 ms where 6 takes 1.33 ms at B = 8,
+// H = 32, n = 8192).
+int ppw_for(int dk) { return dk == 16 ? 6 : 8; }
 
 // Canonical index of the degree-2 feature (a, b), a <= b, among degree-2 features.
 int idx2(int d, int a, int b) { return a * d - a * (a - 1) / 2 + (b - a); }
@@ -1002,7 +1006,7 @@ hipError_t launch_prefill_blocks(const void* q, const void* k, const void* v, vo
   const u16* kk = (const u16*)k;
   const u16* vv = (const u16*)v;
   if (dk == 32) return launch_typed<32, 32, 8>(qq, kk, vv, (u16*)y, S_out, BH, n, chunk, dt, partial, s, qg);
-  return launch_typed<16, 16, 16>(qq, kk, vv, (u16*)y, S_out, BH, n, chunk, dt, partial, s, qg);
+  return launch_typed<16, 16, 6>(qq, kk, vv, (u16*)y, S_out, BH, n, chunk, dt, partial, s, qg);
 }
 
 }  // namespace sata
