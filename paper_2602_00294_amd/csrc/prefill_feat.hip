@@ -328,9 +328,18 @@ prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, cons
           for (int g = 0; g < 4; ++g) {
             asm volatile("" ::: "memory");
             uint2 pw[8];
+            uint64_t pke[8];
             float xa[8], xb[8];
 #pragma unroll
             for (int r = 0; r < 8; ++r) pw[r] = gb[8 * g + r];
+            // with split operands (the float32 path, whose high-P shapes have
+            // many features of degree 4 and up) the group's packed entries,
+            // which supply those features' further indices, are loaded with
+            // its program words rather than when a feature needs them
+            if constexpr (X3) {
+#pragma unroll
+              for (int r = 0; r < 8; ++r) pke[r] = packed[fb0 + 8 * g + r];
+            }
 #pragma unroll
             for (int r = 0; r < 8; ++r) {
               const uint32_t off = pw[r].x & 0x3ffu;
@@ -349,7 +358,9 @@ prefill_feat_main(const void* __restrict__ q_, const void* __restrict__ k_, cons
                 if (W != 1) pq = xq[lane * XS + a0] * xq[lane * XS + a1];
                 if (W != 0) pk = xk[lane * XS + a0] * xk[lane * XS + a1];
                 if ((pw[r].x >> 30) & 1) {
-                  const uint64_t e = packed[fb0 + 8 * g + r];
+                  uint64_t e;
+                  if constexpr (X3) e = pke[r];
+                  else e = packed[fb0 + 8 * g + r];
                   const int p = (int)(e >> 56);
                   auto idx = [&](int j) { return j < p - 1 ? (int)((e >> (8 * j)) & 0xff) : dk; };
                   for (int j = 2; j < p - 1; j += 2) {
