@@ -263,8 +263,10 @@ __device__ __forceinline__ int pk_i1(uint32_t x) { return (x >> 12) & 255; }
 __device__ __forceinline__ int pk_nrows(uint32_t x) { return (x >> 20) & 63; }
 __device__ __forceinline__ int pk_rho_from(uint32_t x) { return (x >> 26) & 63; }
 
-template <int DK, int DV, int NW, int PPW>
-__global__ void __launch_bounds__(NW * 64)
+// DENSE: registers capped for four waves per SIMD (two workgroups per compute
+// unit, a few registers spilled), for calls with workgroups to fill both.
+template <int DK, int DV, int NW, int PPW, bool DENSE>
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(DENSE ? 4 : 1)))
 prefill_blocks_main(const u16* __restrict__ q, const u16* __restrict__ k, const u16* __restrict__ v,
                   const uint2* __restrict__ pmeta, const int* __restrict__ slice_ng,
                   const uint32_t* __restrict__ colmeta_g, const int* __restrict__ zmap,
@@ -964,7 +966,11 @@ template <int DK, int DV, int PPW>
 hipError_t launch_typed(const u16* q, const u16* k, const u16* v, u16* y, float* S_out, int BH, int n, int C,
                         const DeviceTables& dt, float* partial, hipStream_t s, int qg) {
   using L = MainLds<DK, DV, kNW, PPW>;
-  auto kmain = prefill_blocks_main<DK, DV, kNW, PPW>;
+  // two workgroups per compute unit pay where there are workgroups for both
+  // (at d = 16, B = 64, H = 32: 2.69 -> 2.02 ms; at 256 heads, one per compute
+  // unit, the capped registers cost 5%); only where the LDS lets two share one
+  const bool dense = DK == 16 && 2 * L::kBytes <= 160 * 1024 && (int64_t)BH * dt.nslices >= 512;
+  auto kmain = dense ? prefill_blocks_main<DK, DV, kNW, PPW, DK == 16> : prefill_blocks_main<DK, DV, kNW, PPW, false>;
   hipError_t e = hipFuncSetAttribute((const void*)kmain, hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kmain, dim3((unsigned)dt.nslices, (unsigned)BH), dim3(kNW * 64), L::kBytes, s, q, k, v,

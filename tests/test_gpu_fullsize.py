@@ -124,19 +124,19 @@ def test_large_head_d64(sata):
 
 
 def test_large_head_d64_two_segments(sata):
-    """B=2, H=8, n=8192, d=64, bf16: the generated-feature kernel's partial sums
-    (94 slices x 65 floats per head-token) fill its 2 GB segment at 5440
+    """B=2, H=8, n=10240, d=64, bf16: the generated-feature kernel's partial
+    sums (63 slices x 65 floats per head-token) fill its 2 GB segment at 8192
     tokens, so the state is stored and reloaded once; rows on both sides of
     the boundary and after it, then decode steps from the final state."""
-    B, H, n, n_dec, d, P = 2, 8, 8192, 4, 64, 4
+    B, H, n, n_dec, d, P = 2, 8, 10240, 4, 64, 4
     q, k, v = _gen(6, B, H, n + n_dec, d, "bf16")
     ops = operands(sata, "bf16", B, H, n, d, d, P, 64)
     assert ops == "bf16"
     dev = lambda a: to_dev(np.ascontiguousarray(a), "bf16")
-    _say("prefill d=64 n=8192")
+    _say("prefill d=64 n=10240")
     y, S = sata.prefill(dev(q[:, :, :n]), dev(k[:, :, :n]), dev(v[:, :, :n]), P, 64)
     torch.cuda.synchronize()
-    rows = sorted(set(_rows(n, 6)) | {5375, 5376, 5438, 5439, 5440, 5441, 5503, 5504, 8000})
+    rows = sorted(set(_rows(n, 6)) | {8127, 8128, 8190, 8191, 8192, 8193, 8255, 8256, 10000})
     _check_rows(to_host(y), q, k, v, P, [(0, 0), (B - 1, H - 1)], rows, y_tol(ops, "bf16"), "two segments")
     ys = [to_host(sata.decode_step(S, dev(q[:, :, t]), dev(k[:, :, t]), dev(v[:, :, t]), P)) for t in range(n, n + n_dec)]
     torch.cuda.synchronize()
