@@ -97,12 +97,6 @@ hipError_t launch_prefill_generic_readout(const void* q, const void* k, const vo
                                           const PrefillGenericPlan& plan, float* S_state, float* partial, int seg0,
                                           int seg_len, bool first, hipStream_t s);
 
-// One segment of the float32 prefill's finalize: adds nslices partial readouts
-// ([slice][BH][seg_len][d_v+1]), the intra-chunk term, and divides.
-hipError_t launch_prefill_generic_finalize(const void* q, const void* k, const void* v, void* y, bool bf16, int BH,
-                                           int n, int dk, int dv, int P, int chunk, int nslices, int seg0,
-                                           int seg_len, const float* partial, hipStream_t s, int qg);
-
 // ---- prefill, matrix cores with generated features (prefill_feat.hip) ---------
 // Any d_k, d_v <= 64 and P >= 2 with 64-token chunks; state in accumulators.
 struct FeatPrefillPlan {

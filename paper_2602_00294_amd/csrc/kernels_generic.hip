@@ -984,31 +984,4 @@ hipError_t launch_prefill_generic_readout(const void* q, const void* k, const vo
   return hipGetLastError();
 }
 
-hipError_t launch_prefill_generic_finalize(const void* q, const void* k, const void* v, void* y, bool bf16, int BH,
-                                           int n, int dk, int dv, int P, int chunk, int nslices, int seg0,
-                                           int seg_len, const float* partial, hipStream_t s, int qg) {
-  const int C = chunk;
-  const int E = dv + 1;
-  const size_t lds =
-      sizeof(float) * ((size_t)2 * C * fin_stride(dk) + (size_t)C * E + (size_t)kFinRows * C + (size_t)kFinRows * E);
-  const int seg_tokens = std::min(seg_len, n - seg0);
-  dim3 g2((unsigned)((seg_tokens + C - 1) / C), (unsigned)BH);
-  hipError_t e;
-  if (bf16) {
-    if ((e = hipFuncSetAttribute((const void*)prefill_generic_finalize<bf16_t>,
-                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) != hipSuccess)
-      return e;
-    hipLaunchKernelGGL(prefill_generic_finalize<bf16_t>, g2, dim3(kThreads), lds, s, (const bf16_t*)q,
-                       (const bf16_t*)k, (const bf16_t*)v, partial, (bf16_t*)y, BH, n, dk, dv, P, C, nslices, seg0,
-                       seg_len, qg);
-  } else {
-    if ((e = hipFuncSetAttribute((const void*)prefill_generic_finalize<float>,
-                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) != hipSuccess)
-      return e;
-    hipLaunchKernelGGL(prefill_generic_finalize<float>, g2, dim3(kThreads), lds, s, (const float*)q, (const float*)k,
-                       (const float*)v, partial, (float*)y, BH, n, dk, dv, P, C, nslices, seg0, seg_len, qg);
-  }
-  return hipGetLastError();
-}
-
 }  // namespace sata
