@@ -1,6 +1,11 @@
 """Error measures used to compare a result against the oracle (test infrastructure only).
 
-* ``row_rel_error``: per query row, ||y_hat_T - y_T||_2 / ||y_T||_2.  Rows whose
+* ``row_rel_error``: per query row, ||y_hat_T - y_T||_2 / ||y_T||_2, where, when
+  the caller passes the rows' term scales rho_T (``taylor.term_scale``),
+  ||y_T|| is floored at rho_T / CANCEL_FLOOR: a row whose numerator cancels by
+  accident to below a tenth of the size that independent roundings of its
+  terms add up to is judged against that size, as any finite-precision sum of
+  those terms can be off by it.  Rows whose
   denominator nearly cancels (kappa_T > KAPPA_MAX, possible only for even P, where
   the truncated series has a real root) are reported separately and left out of
   the graded maximum; a comparison in which every row would be left out is an
@@ -21,10 +26,11 @@ import math
 
 import numpy as np
 
-__all__ = ["KAPPA_MAX", "TOL_F32", "TOL_BF16", "TOL_F32_ARITH_BF16_OUT", "row_rel_error", "max_row_rel_error",
+__all__ = ["KAPPA_MAX", "CANCEL_FLOOR", "TOL_F32", "TOL_BF16", "TOL_F32_ARITH_BF16_OUT", "row_rel_error", "max_row_rel_error",
            "state_rel_error", "state_elem_error", "state_tol", "y_tol", "log10_abs_diff"]
 
 KAPPA_MAX = 100.0
+CANCEL_FLOOR = 10.0
 TOL_F32 = 1e-4
 TOL_BF16 = 2e-2
 # float32 arithmetic whose output is stored in bfloat16: the storage rounding
@@ -35,20 +41,24 @@ _U32 = 2.0 ** -24  # unit roundoff of float32
 _UBF16 = 2.0 ** -8  # unit roundoff of bfloat16 (8 significant bits)
 
 
-def row_rel_error(y_hat, y) -> np.ndarray:
+def row_rel_error(y_hat, y, scale=None) -> np.ndarray:
+    """||y_hat_T - y_T|| / max(||y_T||, scale_T / CANCEL_FLOOR) per row (plain
+    ||y_T|| when scale is None)."""
     y_hat = np.asarray(y_hat, dtype=np.float64)
     y = np.asarray(y, dtype=np.float64)
     num = np.linalg.norm(y_hat - y, axis=-1)
     den = np.linalg.norm(y, axis=-1)
+    if scale is not None:
+        den = np.maximum(den, np.asarray(scale, dtype=np.float64) / CANCEL_FLOOR)
     return num / den
 
 
-def max_row_rel_error(y_hat, y, kappa=None):
+def max_row_rel_error(y_hat, y, kappa=None, scale=None):
     """(max error over well-conditioned rows, number of excluded rows).
 
     Raises ValueError when there is no row to grade (no rows at all, or every
     row excluded by kappa), so that such a comparison cannot pass vacuously."""
-    err = row_rel_error(y_hat, y)
+    err = row_rel_error(y_hat, y, scale)
     if err.size == 0:
         raise ValueError("no rows to compare")
     if kappa is None:

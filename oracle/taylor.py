@@ -21,6 +21,10 @@ What is computed (sections of the paper in brackets):
                         f_P(q_T . k_t / sqrt(d_k)) for t <= T (inclusive), then
                         numerator / denominator [App. A2, the causal output
                         y_T and its Taylor substitution].
+* ``term_scale``        the root-sum-square size of a row's terms w_Tt v_t over
+                        |Z_T|: the size that roundings of independent signs
+                        add up to, below which a row's numerator has cancelled
+                        by accident [App. A2, the causal output y_T].
 * ``softmax_attention`` the exact causal softmax attention it approximates
                         [App. A2, first display].
 * ``multi_indices`` / ``multiplicity`` / ``phi_ref``
@@ -69,12 +73,13 @@ from __future__ import annotations
 
 import itertools
 import math
-from typing import Iterable, List, Sequence, Tuple
+from typing import Iterable, List, Optional, Sequence, Tuple
 
 import numpy as np
 
 __all__ = [
-    "taylor_poly", "taylor_attention", "taylor_attention_rows", "taylor_attention_backward", "softmax_attention",
+    "taylor_poly", "taylor_attention", "taylor_attention_rows", "term_scale", "taylor_attention_backward",
+    "softmax_attention",
     "softmax_attention_rows", "multi_indices", "multiplicity", "alpha", "feature_weights",
     "phi_ref", "state_ref", "state_abs_ref", "readout_ref", "recurrent_attention", "decode_ref",
     "feature_count", "degree_count", "state_elems", "flops_per_token",
@@ -192,6 +197,35 @@ def taylor_attention_rows(q, k, v, P: int, rows: Sequence[int]):
         Z[i] = den
         kappa[i] = np.abs(w).sum() / abs(den)
     return y, Z, kappa
+
+
+def term_scale(q, k, v, P: int, rows: Optional[Sequence[int]] = None) -> np.ndarray:
+    """rho_T = sqrt(sum_{t <= T} w_Tt^2 ||v_t||^2) / |Z_T| per query row T
+    (every row when rows is None), with w_Tt and Z_T as in taylor_attention.
+
+    y_T is a sum of the terms w_Tt v_t / Z_T; roundings of independent signs in
+    those terms add up to about rho_T times the unit roundoff, whatever the
+    size of the sum.  A row whose numerator cancels by accident has
+    ||y_T|| far below rho_T; the row error measure floors ||y_T|| at a fixed
+    fraction of rho_T (metrics.row_rel_error)."""
+    q, k, v = _as64(q), _as64(k), _as64(v)
+    n, d_k = q.shape
+    c = math.sqrt(d_k)
+    vv = (v * v).sum(axis=1)                                # ||v_t||^2
+    if rows is None:                                        # all rows, blocked by query rows
+        out = np.empty(n)
+        for r0 in range(0, n, 512):
+            r1 = min(n, r0 + 512)
+            w = taylor_poly((q[r0:r1] @ k[:r1].T) / c, P)
+            w = np.where(np.arange(r1)[None, :] <= np.arange(r0, r1)[:, None], w, 0.0)
+            out[r0:r1] = np.sqrt((w * w) @ vv[:r1]) / np.abs(w.sum(axis=1))
+        return out
+    rows = list(rows)
+    out = np.empty(len(rows))
+    for i, T in enumerate(rows):
+        w = taylor_poly((k[: T + 1] @ q[T]) / c, P)
+        out[i] = math.sqrt(float((w * w) @ vv[: T + 1])) / abs(w.sum())
+    return out
 
 
 def taylor_attention_backward(q, k, v, dy, P: int, block: int = 512):

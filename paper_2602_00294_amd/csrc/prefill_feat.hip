@@ -25,8 +25,9 @@
 // fit).  The readout uses the state before the chunk's update, so the
 // inter-chunk term is exactly phi(Q_c) S_{c-1}.  The waves' partial readouts
 // are added in wave order through LDS and the slice's partial row written per
-// token; a second kernel adds the slices' partials in slice order and the
-// float32 prefill's finalize kernel adds the intra-chunk term and divides.
+// token; a second kernel adds the slices' partials in slice order and a
+// finalize kernel (on the float32 matrix-core products) adds the intra-chunk
+// term and divides.
 //
 // Operand layouts (16 x 16 x 32 bf16): A lane l holds row l % 16 and K entries
 // 8 (l / 16) .. +7; B lane l holds column l % 16 and the same K entries; the

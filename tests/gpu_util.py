@@ -37,15 +37,17 @@ def operands(sata, dtype, B, H, n, dk, dv, P, chunk):
     return sata.prefill_operands(torch_dtype(dtype), B, H, n, dk, dv, P, chunk)
 
 
-def check_rows(y_gpu, y_ref, kappa, tol, P, label=""):
+def check_rows(y_gpu, y_ref, kappa, tol, P, label="", scale=None):
     """Rows of one head against the oracle.  Rows whose denominator cancels
     (kappa > KAPPA_MAX, possible for even P only) are reported and left out;
     every other row must be finite and within `tol`.  For odd P no row may be
-    left out, and at least one row is always graded.  Returns (error, excluded)."""
+    left out, and at least one row is always graded.  With the rows' term
+    scales (oracle.term_scale), a row whose numerator has cancelled by accident
+    is judged against a tenth of that scale.  Returns (error, excluded)."""
     y_gpu = np.asarray(y_gpu)
     kappa = np.asarray(kappa)
     assert np.all(np.isfinite(y_gpu[kappa <= KAPPA_MAX])), f"{label}: non-finite well-conditioned row"
-    err, excluded = max_row_rel_error(y_gpu, y_ref, kappa)
+    err, excluded = max_row_rel_error(y_gpu, y_ref, kappa, scale)
     if P % 2 == 1:
         assert excluded == 0, f"{label}: {excluded} rows excluded at odd P={P}"
     assert err <= tol, f"{label}: max row rel error {err:.3e} > {tol:.1e} (excluded {excluded})"
@@ -71,7 +73,7 @@ def check_prefill_head(y_gpu, S_gpu, q, k, v, P, ops, out_dtype, chunk, label=""
 
     Returns (max row error, excluded rows, state error or None)."""
     y_ref, _, kappa = oracle.taylor_attention(q, k, v, P)
-    err, excluded = check_rows(y_gpu, y_ref, kappa, y_tol(ops, out_dtype), P, label)
+    err, excluded = check_rows(y_gpu, y_ref, kappa, y_tol(ops, out_dtype), P, label, oracle.term_scale(q, k, v, P))
     s_err = None
     if S_gpu is not None:
         s_err = check_state(S_gpu, k, v, P, ops, q.shape[0], chunk, label)

@@ -39,6 +39,52 @@ def test_max_row_rel_error_counts_and_refuses_empty():
         me.max_row_rel_error(np.zeros((0, 2)), np.zeros((0, 2)))
 
 
+def test_row_rel_error_floor_hand_values():
+    """With term scales rho, ||y_T|| is floored at rho_T / 10: row 0 (norm 5)
+    is left alone by rho = 20, row 1 (norm 1) is judged against 30 / 10 = 3,
+    and row 2 (an exactly cancelled numerator, norm 0) against 50 / 10 = 5."""
+    y = np.array([[3.0, 4.0], [1.0, 0.0], [0.0, 0.0]])
+    y_hat = np.array([[3.0, 5.0], [1.0, 1.5], [0.0, 0.5]])
+    assert me.CANCEL_FLOOR == 10.0
+    np.testing.assert_allclose(me.row_rel_error(y_hat, y, scale=[20.0, 30.0, 50.0]), [0.2, 0.5, 0.1], rtol=1e-15)
+    assert me.max_row_rel_error(y_hat, y, kappa=[1.0, 1.0, 1.0], scale=[20.0, 30.0, 50.0]) == (0.5, 0)
+    # without scales the cancelled row has no finite relative error
+    with np.errstate(divide="ignore"):
+        assert math.isinf(me.row_rel_error(y_hat, y)[2])
+
+
+def test_term_scale_closed_forms():
+    """P = 1 makes every weight 1: rho_T = sqrt(sum_{t<=T} ||v_t||^2) / (T + 1).
+    P = 2 makes the weights 1 + q_T.k_t / sqrt(d), written out here with a loop
+    over tokens; both with and without a row list."""
+    rng = np.random.default_rng(17)
+    q, k, v = rng.standard_normal((9, 3)), rng.standard_normal((9, 3)), rng.standard_normal((9, 2))
+    vv = np.cumsum((v ** 2).sum(axis=1))
+    np.testing.assert_allclose(oracle.term_scale(q, k, v, 1), np.sqrt(vv) / np.arange(1, 10), rtol=1e-14)
+    want = []
+    for T in range(9):
+        w = [1.0 + float(np.dot(q[T], k[t])) / math.sqrt(3.0) for t in range(T + 1)]
+        want.append(math.sqrt(sum(w[t] ** 2 * float(np.dot(v[t], v[t])) for t in range(T + 1))) / abs(sum(w)))
+    np.testing.assert_allclose(oracle.term_scale(q, k, v, 2), want, rtol=1e-13)
+    np.testing.assert_allclose(oracle.term_scale(q, k, v, 2, rows=[8, 2]), [want[8], want[2]], rtol=1e-13)
+
+
+def test_term_scale_floor_leaves_one_term_rows_alone():
+    """A row with a single term (T = 0) has ||y_0|| = ||v_0|| = rho_0, ten
+    times the floor, so the floor never binds there; for non-negative weights
+    and values ||y_T|| >= rho_T (the norm of a sum of non-negative vectors is
+    at least the root-sum-square of their norms), so it never binds either."""
+    rng = np.random.default_rng(3)
+    q, k = rng.standard_normal((40, 4)), rng.standard_normal((40, 4))
+    v = np.abs(rng.standard_normal((40, 5)))
+    y, _, _ = oracle.taylor_attention(q, k, v, 3)
+    rho = oracle.term_scale(q, k, v, 3)
+    assert np.all(np.linalg.norm(y, axis=1) >= rho * (1 - 1e-12))
+    np.testing.assert_allclose(rho[0], np.linalg.norm(v[0]), rtol=1e-14)
+    y_hat = y * (1 + 1e-3)
+    np.testing.assert_array_equal(me.row_rel_error(y_hat, y, rho), me.row_rel_error(y_hat, y))
+
+
 def test_state_rel_error_hand_value():
     assert me.state_rel_error([[3.0, 5.0]], [[3.0, 4.0]]) == pytest.approx(0.2, rel=1e-15)
 
