@@ -1,5 +1,7 @@
-"""GPU parity over a seeded draw of shapes: prefill (output and state), then
-a few decode steps that continue it, each against the float64 oracle.
+"""GPU parity over seeded draws of shapes: prefill (output and state), then
+a few decode steps that continue it, each against the float64 oracle; and
+the same for grouped query heads (prefill and decode of G query heads per
+key/value head).
 
 The fixed cases of the other files pin one kernel family each; this draw
 mixes the arguments they leave uncrossed (d_k != d_v, every chunk size,
@@ -90,3 +92,64 @@ def test_prefill_then_decode_matches_oracle(sata, case):
             check_rows(got, yr, kap, y_tol(ops, dtype), P, f"{case} decode b{b} h{h}", rho)
             check_state(S_host[b, h], k[b, h], v[b, h], P, ops, n, chunk, f"{case} decoded state b{b} h{h}",
                         steps=steps)
+
+
+def _draw_grouped_cases(seed=2603, count=12):
+    """(workload, B, H_kv, G, n, d_k, d_v, P, chunk, dtype) tuples for the
+    grouped prefill and decode, under the same oracle budget."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < count:
+        chunk = int(rng.choice([16, 32, 64, 64]))
+        dk = int(rng.integers(1, 65))
+        dv = int(rng.integers(1, 65))
+        P = int(rng.integers(1, 7))
+        D = comb(dk + P - 1, P - 1)
+        if D > 60000:
+            continue
+        long_seq = rng.random() < 0.25
+        n = int(rng.integers(2048, 4200)) if long_seq else int(rng.integers(1, 500))
+        if n * D * max(P - 1, 1) > 2e7:
+            continue
+        G = int(rng.choice([2, 4, 8]))
+        Hkv = 1 if long_seq else int(rng.integers(1, 3))
+        B = int(rng.integers(1, 3))
+        dtype = "bf16" if rng.random() < 0.5 else "f32"
+        cases.append((300 + len(cases), B, Hkv, G, n, dk, dv, P, chunk, dtype))
+    return cases
+
+
+GROUPED_CASES = _draw_grouped_cases()
+
+
+@pytest.mark.parametrize("case", GROUPED_CASES, ids=lambda c: "w{}_B{}Hkv{}G{}n{}dk{}dv{}P{}C{}_{}".format(*c))
+def test_grouped_prefill_then_decode_matches_oracle(sata, case):
+    """Query head g + G h against the oracle on its own queries and key/value
+    head h's tokens, through the grouped prefill and two grouped decode steps."""
+    workload, B, Hkv, G, n, dk, dv, P, chunk, dtype = case
+    steps = 2
+    print(f"random grouped shape {case} D={comb(dk + P - 1, P - 1)}", file=sys.stderr, flush=True)
+    q, _, _ = syn.make_qkv(workload, B, Hkv * G, n + steps, dk, dv, dtype)
+    _, k, v = syn.make_qkv(workload + 1000, B, Hkv, n + steps, dk, dv, dtype)
+    dev = lambda a: to_dev(np.ascontiguousarray(a), dtype)
+    ops = operands(sata, dtype, B, Hkv, n, dk, dv, P, chunk)
+    y, S = sata.prefill_grouped(dev(q[:, :, :n]), dev(k[:, :, :n]), dev(v[:, :, :n]), P, chunk)
+    torch.cuda.synchronize()
+    yh = to_host(y)
+    ys = [to_host(sata.decode_step_grouped(S, dev(q[:, :, t]), dev(k[:, :, t]), dev(v[:, :, t]), P))
+          for t in range(n, n + steps)]
+    torch.cuda.synchronize()
+    S_host = to_host(S)
+    tol = y_tol(ops, dtype)
+    for b in range(B):
+        for hq in range(Hkv * G):
+            h = hq // G
+            label = f"{case} b{b} query head {hq}"
+            yr, _, kap = oracle.taylor_attention(q[b, hq, :n], k[b, h, :n], v[b, h, :n], P)
+            check_rows(yh[b, hq], yr, kap, tol, P, label, oracle.term_scale(q[b, hq, :n], k[b, h, :n], v[b, h, :n], P))
+            rows = list(range(n, n + steps))
+            yr, _, kap = oracle.taylor_attention_rows(q[b, hq], k[b, h], v[b, h], P, rows)
+            got = np.stack([yy[b, hq] for yy in ys])
+            check_rows(got, yr, kap, tol, P, label + " decode", oracle.term_scale(q[b, hq], k[b, h], v[b, h], P, rows))
+        for h in range(Hkv):
+            check_state(S_host[b, h], k[b, h], v[b, h], P, ops, n, chunk, f"{case} state b{b} h{h}", steps=steps)
