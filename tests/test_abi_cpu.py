@@ -251,3 +251,22 @@ class TestBindingRejectsBeforeLaunch:
             bnd.decode_step_grouped(S, q, k, v, 3, y=self.t(1, 2, 5))
         with pytest.raises(ValueError, match="GPU"):
             bnd.decode_step_grouped(S, q, k, v, 3)
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    """No fallback: without the built library the binding raises before any work."""
+    with pytest.raises(RuntimeError, match="missing"):
+        bnd.load_library(str(tmp_path / "libsata.so"))
+
+
+def test_product_path_does_not_touch_the_oracle():
+    """The package's Python and HIP sources never import, load or name the
+    oracle: every result comes from the library's kernels."""
+    import pathlib
+    import re
+    pkg = pathlib.Path(bnd.__file__).resolve().parent
+    sources = [p for p in pkg.rglob("*") if p.suffix in (".py", ".hip", ".hpp", ".h", ".cpp")]
+    assert sources
+    for p in sources:
+        text = p.read_text()
+        assert not re.search(r"\boracle\b", text), f"{p} names the oracle"
