@@ -163,15 +163,23 @@ def _features(d: int, P: int) -> int:
     return D
 
 
-def feature_map(x, P: int):
-    """phi(x) for x [..., d] (float32 or bfloat16) -> float32 [..., D]."""
+def feature_map(x, P: int, phi=None):
+    """phi(x) for x [..., d] (float32 or bfloat16) -> float32 [..., D].
+
+    A preallocated float32 output [..., D] may be passed as phi=."""
     torch = _torch()
     code = _dtype_code(x)
     d = x.shape[-1]
     rows = x.numel() // d if d else 0
     D = _features(d, P)
+    if phi is not None:
+        if phi.dtype != torch.float32:
+            raise TypeError(f"phi is {phi.dtype}, expected torch.float32")
+        _check_shape(phi, "phi", (*x.shape[:-1], D))
     _check_tensor(x, "x")
-    phi = torch.empty(*x.shape[:-1], D, dtype=torch.float32, device=x.device)
+    if phi is None:
+        phi = torch.empty(*x.shape[:-1], D, dtype=torch.float32, device=x.device)
+    _check_tensor(phi, "phi", x.device)
     with torch.cuda.device(x.device):
         _check(load_library().sata_feature_map(_ptr(x), code, rows, d, P, _ptr(phi), _stream_ptr()),
                "sata_feature_map")

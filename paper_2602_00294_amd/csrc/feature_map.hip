@@ -3,7 +3,8 @@
 // indices' coordinates.  The kernel is bound by the HBM writes of the
 // float32 output, D / d times the input.
 //
-// A workgroup takes kRows rows and 256 consecutive features (one per thread).
+// A workgroup takes kRows rows and 256 consecutive features (one per thread);
+// workgroups that write the same rows run on one XCD (see the tile remap).
 // Each thread reads its feature's generation-program word once (x offset of
 // the last index, the first two other indices, a flag for more, the weight;
 // table.hpp build_gen_program), so a row costs three LDS reads, three
@@ -30,7 +31,21 @@ __global__ void __launch_bounds__(kFmThreads)
 feature_map_kernel(const T* __restrict__ x, int64_t rows, int d, const uint32_t* __restrict__ gen,
                    const uint64_t* __restrict__ packed, int64_t D, float* __restrict__ phi) {
   extern __shared__ float xt[];  // [d + 1][kXT]
-  const int64_t r0 = (int64_t)blockIdx.y * kRows;
+  // workgroups are dealt to the 8 XCDs in turn by linear index; with more
+  // than one feature block per row, the remap gives each XCD a contiguous run
+  // of (row block, feature block) tiles, so that the neighbouring feature
+  // blocks of a row, which share the cache lines at their edges, are written
+  // through the same L2 (one feature block writes whole rows: no remap)
+  int64_t rb = blockIdx.y, fb = 0;
+  if (gridDim.x > 1) {
+    const int64_t nblk = (int64_t)gridDim.x * gridDim.y;
+    const int64_t lin = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+    const int64_t per_xcd = nblk / 8;
+    const int64_t tile = lin < 8 * per_xcd ? (lin % 8) * per_xcd + lin / 8 : lin;
+    rb = tile / gridDim.x;
+    fb = tile % gridDim.x;
+  }
+  const int64_t r0 = rb * kRows;
   const int nr = (int)min<int64_t>(kRows, rows - r0);
   const int tid = threadIdx.x;
   for (int i = tid; i < kRows * d; i += kFmThreads) {
@@ -40,7 +55,7 @@ feature_map_kernel(const T* __restrict__ x, int64_t rows, int d, const uint32_t*
   }
   for (int r = tid; r < kRows; r += kFmThreads) xt[d * kXT + r] = 1.f;
   __syncthreads();
-  const int64_t f = (int64_t)blockIdx.x * kFmThreads + tid;
+  const int64_t f = fb * kFmThreads + tid;
   if (f >= D) return;
   const uint32_t w0 = gen[2 * f];
   const float w = __uint_as_float(gen[2 * f + 1]);

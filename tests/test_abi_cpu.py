@@ -194,6 +194,13 @@ class TestBindingRejectsBeforeLaunch:
     def t(self, *shape, dtype=None):
         return self.torch.zeros(*shape, dtype=dtype or self.torch.float32)
 
+    def test_feature_map_output(self):
+        x = self.t(5, 3)                                      # D = 10 at d=3, P=3
+        with pytest.raises(TypeError):
+            bnd.feature_map(x, 3, phi=self.t(5, 10, dtype=self.torch.bfloat16))
+        with pytest.raises(ValueError):
+            bnd.feature_map(x, 3, phi=self.t(5, 9))
+
     def test_prefill(self):
         bf = self.torch.bfloat16
         q, k, v = self.t(1, 2, 8, 4), self.t(1, 2, 8, 4), self.t(1, 2, 8, 3)

@@ -54,6 +54,25 @@ def test_feature_map(sata, d, P, rows, dtype):
     np.testing.assert_allclose(phi, ref, rtol=2e-6, atol=1e-30)
 
 
+def test_feature_map_unaligned_output(sata):
+    """An output pointer that is not 16-byte aligned (the C ABI allows any
+    float pointer) takes element stores; the elements around it stay untouched."""
+    import ctypes
+    d, P, rows = 6, 4, 50
+    D = oracle.feature_count(d, P)
+    x = syn.head_stream(101, d, P, 0, (rows, d), "f32")
+    xd = to_dev(x, "f32")
+    buf = torch.full((rows * D + 8,), -7.0, device="cuda")
+    lib = sata.load_library()
+    st = lib.sata_feature_map(ctypes.c_void_p(xd.data_ptr()), 0, rows, d, P, ctypes.c_void_p(buf.data_ptr() + 4),
+                              ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    torch.cuda.synchronize()
+    assert st == 0
+    b = to_host(buf)
+    assert b[0] == -7.0 and np.all(b[1 + rows * D:] == -7.0)
+    np.testing.assert_allclose(b[1:1 + rows * D].reshape(rows, D), oracle.phi_ref(x, P), rtol=2e-6, atol=1e-30)
+
+
 # ------------------------------------------------------------------ prefill
 
 def _run_prefill(sata, workload, B, H, n, dk, dv, P, chunk, dtype, want_state=True):
