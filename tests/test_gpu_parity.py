@@ -54,6 +54,23 @@ def test_feature_map(sata, d, P, rows, dtype):
     np.testing.assert_allclose(phi, ref, rtol=2e-6, atol=1e-30)
 
 
+def test_feature_map_many_row_blocks_and_feature_blocks(sata):
+    """Several feature blocks per row (D = 561) over more row blocks than one
+    launch takes (65535 blocks of 32 rows): the XCD-ordered tiles of every
+    launch cover each output once.  Sampled rows: the first, those around the
+    launch boundary (row 65535 * 32) and the last."""
+    d, P, rows = 32, 3, 2_100_000
+    D = oracle.feature_count(d, P)
+    x = syn.head_stream(102, d, P, 0, (rows, d), "f32")
+    phi = sata.feature_map(to_dev(x, "f32"), P)
+    torch.cuda.synchronize()
+    b = 65535 * 32
+    idx = np.r_[0:40, b - 40:b + 40, rows - 40:rows]
+    got = to_host(phi[torch.from_numpy(idx).cuda()])
+    np.testing.assert_allclose(got, oracle.phi_ref(x[idx], P), rtol=2e-6, atol=1e-30)
+    assert bool(torch.isfinite(phi).all())
+
+
 def test_feature_map_unaligned_output(sata):
     """An output pointer that is not 16-byte aligned (the C ABI allows any
     float pointer) takes element stores; the elements around it stay untouched."""
